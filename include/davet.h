@@ -1,0 +1,288 @@
+/*
+ * davet.h -- C ABI of the DAVET per-denoising-step hot path on MI355X (gfx950).
+ *
+ * DAVET (Denoising-Aware Visual Evidence Trajectory Allocation) conditions each
+ * denoising step of a diffusion vision-language model on one of K evidence views
+ * built once from a single visual encoding, chosen per step by an allocation
+ * policy.  This library implements, for one GPU:
+ *
+ *   davet_build_views    the ordered evidence hierarchy (Sec. 4.3)
+ *   davet_denoise_step   one pass of the bidirectional denoiser over
+ *                        [view | prompt | response] (Sec. 3.1, Eq. 1) with the
+ *                        argmax / confidence decoding of masked positions
+ *   davet_unmask         confidence-ranked commitment (Eq. 2)
+ *   davet_policy_*       the allocation policy (Sec. 4.2, Eqs. 6-9), host-side
+ *   davet_run_schedule   the whole loop: views once, then T steps
+ *
+ * Conventions, for every entry point:
+ *   - Pointers are DEVICE pointers unless the comment says host.  Arrays are
+ *     dense and row-major.  The caller owns every buffer, including the
+ *     workspace; the library never frees caller memory and allocates no device
+ *     memory (davet_run_schedule may use small host-side vectors).
+ *   - Device work is enqueued asynchronously on the given HIP stream.  Only
+ *     davet_run_schedule in policy mode synchronises (one small device-to-host
+ *     copy per step, to read the signals the risk of the next step needs).
+ *   - Every argument is validated before anything is enqueued; on an error the
+ *     call returns a negative davet_status, enqueues nothing, and
+ *     davet_last_error() describes the failure (thread-local string).
+ *   - Element types: DAVET_F32 = IEEE float32, DAVET_BF16 = bfloat16 bit
+ *     patterns (uint16).  Residual streams, softmax and norms run in float32
+ *     in both modes; bf16 mode feeds bf16 operands to the matrix cores.
+ */
+#ifndef DAVET_H
+#define DAVET_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum davet_status {
+  DAVET_OK = 0,
+  DAVET_EINVAL = -1,   /* bad scalar argument or null pointer              */
+  DAVET_ESHAPE = -2,   /* unsupported or inconsistent shape                 */
+  DAVET_EDTYPE = -3,   /* unsupported element type                          */
+  DAVET_ENOMEM = -4,   /* workspace smaller than davet_workspace_bytes()   */
+  DAVET_EHIP = -5      /* a HIP runtime call failed                         */
+} davet_status;
+
+typedef enum davet_dtype { DAVET_F32 = 0, DAVET_BF16 = 1 } davet_dtype;
+
+/* Limits of this build. */
+#define DAVET_MAX_SEQS 64        /* sequences per packed batch            */
+#define DAVET_MAX_LEVELS 4       /* K                                     */
+#define DAVET_MAX_RESP 1024      /* response length L                     */
+
+/* Geometry of one sample's visual encoding v: n_crops crops of grid x grid
+ * tokens, each token a d-vector; v is [n_crops*grid*grid, d], crop-major, then
+ * row-major inside a crop.  K ordered levels, level K-1 being v itself. */
+typedef struct davet_view_geom {
+  int32_t n_crops;
+  int32_t grid;
+  int32_t d;
+  int32_t K;          /* 1..DAVET_MAX_LEVELS */
+  int32_t dtype;      /* davet_dtype of v and of the pooled levels */
+} davet_view_geom;
+
+/* Denoiser shape.  d = n_heads * head_dim, head_dim in {64, 128}; d and ffn
+ * multiples of 256 (bf16) or 64 (f32); mask_id in [0, vocab). */
+typedef struct davet_model_cfg {
+  int32_t n_layers;
+  int32_t d;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t ffn;
+  int32_t vocab;
+  int32_t mask_id;
+  float rms_eps;
+  float rope_theta;
+  int32_t dtype;      /* davet_dtype of weights, embeddings and views */
+} davet_model_cfg;
+
+/* One layer's parameters (element type = cfg.dtype, out = x W^T):
+ *   wqkv [3d, d]  rows: query heads, key heads, value heads (head-major)
+ *   wo   [d, d]
+ *   wg   [ffn, d] gate, wu [ffn, d] up, wd [d, ffn] down (SwiGLU)
+ *   attn_norm, ffn_norm: float32 [d] RMSNorm gains, or NULL for all-ones. */
+typedef struct davet_layer_weights {
+  const void* wqkv;
+  const void* wo;
+  const void* wg;
+  const void* wu;
+  const void* wd;
+  const float* attn_norm;
+  const float* ffn_norm;
+} davet_layer_weights;
+
+/* embed [vocab, d] token embedding; head [vocab, d] untied output head;
+ * final_norm float32 [d] or NULL; layers: HOST array of n_layers entries. */
+typedef struct davet_weights {
+  const void* embed;
+  const void* head;
+  const float* final_norm;
+  const davet_layer_weights* layers;
+} davet_weights;
+
+/* Allocation policy parameters (Sec. 4.2): average budget B, reserve fraction
+ * rho, risk strength alpha, operation demand d(o) in [0,1], phase orientation
+ * (early != 0: p_t = 1-(t-0.5)/T; else p_t = (t-0.5)/T), K levels. */
+typedef struct davet_policy {
+  double B;
+  double rho;
+  double alpha;
+  double demand;
+  int32_t early;
+  int32_t K;
+} davet_policy;
+
+const char* davet_last_error(void);
+const char* davet_version(void);
+
+/* ---------------------------------------------------------------- views -- */
+
+/* Token counts of the K levels of a geometry (host out[K]).  Level l pools
+ * windows of side 2^(K-1-l) per crop with ceil padding:
+ * n_l = n_crops * ceil(grid / 2^(K-1-l))^2. */
+int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens /*host[K]*/);
+
+/* Evidence hierarchy (Sec. 4.3, "Ordered evidence hierarchy"; Sec. 3.2: a full
+ * budget leaves v unchanged).  Level l < K-1 token j is the mean of the
+ * in-bounds tokens of its window (divisor = member count), accumulated in
+ * float64 and rounded once to the view dtype.  Level K-1 is v itself: nothing
+ * is written for it except its (identity) index map.
+ *   v            [n_crops*grid*grid, d] (dtype g.dtype), read only
+ *   levels       HOST array of K device pointers; levels[l] receives
+ *                [n_l, d] for l < K-1; levels[K-1] is ignored (may be NULL)
+ *   idx_offsets  HOST array of K device pointers (int32 [n_l + 1]) or NULL;
+ *   idx_members  HOST array of K device pointers (int32 [n_crops*grid*grid])
+ *                or NULL.  CSR map: token j of level l pools rows
+ *                members[offsets[j] .. offsets[j+1]) of v, listed row-major in
+ *                the window, ids c*grid*grid + r*grid + s.  Individual entries
+ *                may be NULL to skip that level's map.
+ * Errors: EINVAL (null v / levels entry), ESHAPE (grid<1, n_crops<1, K out of
+ * range, d % 8 != 0), EDTYPE. */
+int davet_build_views(const davet_view_geom* g, const void* v,
+                      void* const* levels, int32_t* const* idx_offsets,
+                      int32_t* const* idx_members, hipStream_t stream);
+
+/* ------------------------------------------------------------- denoiser -- */
+
+/* Workspace bytes davet_denoise_step needs for at most max_tokens packed
+ * tokens (sum over sequences of n_view + prompt + L), max_seqs sequences and
+ * response length L.  The workspace must be 256-byte aligned. */
+int davet_workspace_bytes(const davet_model_cfg* cfg, int32_t max_tokens,
+                          int32_t max_seqs, int32_t L, size_t* bytes /*host*/);
+
+/* One denoising step for a packed batch of n_seqs independent sequences
+ * (Sec. 3.1, Eq. 1, with the view v_t of Sec. 3.2).  Sequence s is
+ *   [ view_ptrs[s] (n_view[s] rows) | E[prompt ids cu_prompt[s]..cu_prompt[s+1]) |
+ *     E[resp_ids[s*L + i]], or E[mask_id] where resp_masked[s*L + i] != 0 ]
+ * at rotary positions 0..N_s-1, run through cfg.n_layers pre-norm layers with
+ * NON-causal attention inside each sequence only (Sec. 1: bidirectional).
+ * For every masked response position the final-normed hidden state is projected
+ * on the vocabulary and decoded at temperature 0 (Sec. 5.1):
+ *   argmax_out[s*L+i] = argmax over w != mask_id (lowest id on ties)
+ *   conf_out[s*L+i]   = max softmax probability, [MASK] excluded from the
+ *                       normaliser: 1 / sum_{w != mask} exp(l_w - l_argmax)
+ * Committed (unmasked) positions get conf = -inf and argmax = -1.
+ *   view_ptrs, n_view, cu_prompt: HOST arrays; view rows have dtype cfg.dtype.
+ *   prompt_ids int32 [cu_prompt[n_seqs]]; resp_ids int32 [n_seqs*L];
+ *   resp_masked uint8 [n_seqs*L]; conf_out float [n_seqs*L];
+ *   argmax_out int32 [n_seqs*L];
+ *   logits_out float [n_seqs*L, vocab] or NULL: when given, the logits of
+ *   masked positions are stored in their rows (other rows untouched).
+ * Errors: EINVAL, ESHAPE (head_dim, d, ffn, n_seqs, L or token counts out of
+ * range), EDTYPE, ENOMEM (ws_bytes too small or workspace misaligned). */
+int davet_denoise_step(const davet_model_cfg* cfg, const davet_weights* w,
+                       int32_t n_seqs, const void* const* view_ptrs,
+                       const int32_t* n_view, const int32_t* prompt_ids,
+                       const int32_t* cu_prompt, const int32_t* resp_ids,
+                       const uint8_t* resp_masked, int32_t L, float* conf_out,
+                       int32_t* argmax_out, float* logits_out, void* workspace,
+                       size_t ws_bytes, hipStream_t stream);
+
+/* --------------------------------------------------------------- unmask -- */
+
+/* Confidence-ranked commitment, Eq. (2) (Sec. 5.1: confidence ranking).  Per
+ * sequence s, among positions with resp_masked != 0, the k_s = min(k, |M|)
+ * positions ranked first by (conf descending, position ascending) -- NaN ranks
+ * with -inf, below every number -- are committed: resp_ids[i] = argmax[i],
+ * resp_masked[i] = 0.  Other positions are untouched.
+ *   conf float [n_seqs*L], argmax int32 [n_seqs*L] (read only)
+ *   resp_ids int32 [n_seqs*L], resp_masked uint8 [n_seqs*L] (updated in place)
+ *   selected int32 [n_seqs*k] or NULL: committed positions of each sequence in
+ *   rank order, padded with -1.
+ * Errors: EINVAL (k < 1, null pointers), ESHAPE (L out of range, n_seqs < 1). */
+int davet_unmask(int32_t n_seqs, int32_t L, int32_t k, const float* conf,
+                 const int32_t* argmax, int32_t* resp_ids, uint8_t* resp_masked,
+                 int32_t* selected, hipStream_t stream);
+
+/* ------------------------------------------------------ policy (host) -- */
+
+/* Demand prior d(o) of Appendix A, Table A: category 0 lexical readout 1.000,
+ * 1 numerical reasoning 0.941, 2 entity grounding 0.824, 3 binary decision
+ * 0.647, 4 general understanding 0.529.  Returns a negative value for an
+ * unknown category. */
+double davet_demand_prior(int32_t category);
+
+/* Evidence envelope, Eq. (6): lower = N(p; (1-rho)B), upper = N(p;
+ * [1-rho+rho d]B), with p the phase profile of Sec. 4.2 and N the rescale-and-
+ * clip normaliser (exact scale: min(1, s p_t), mean = beta; beta >= 1 gives
+ * ones, beta <= 0 zeros).  Double precision, evaluated without contraction.
+ * lower, upper: HOST double [T].  Errors: EINVAL (T < 1, null, non-finite). */
+int davet_policy_envelope(const davet_policy* pol, int32_t T,
+                          double* lower, double* upper);
+
+/* Budget and level of step t (1-based): r_t by Eq. (7) (r_1 = 1), b_t by
+ * Eq. (8), level by Eq. (9) generalised to K levels (count of thresholds j/K,
+ * j = 1..K-1, that are <= b_t).  lower/upper from davet_policy_envelope.
+ * b_t, level, r_t: HOST outputs (r_t may be NULL). */
+int davet_policy_step(const davet_policy* pol, int32_t t, int32_t T,
+                      const double* lower, const double* upper,
+                      double cbar_prev, double churn_prev, double* b_t,
+                      int32_t* level, double* r_t);
+
+/* Generation-state signals after a step (Sec. 4.2, before Eq. 7), all HOST
+ * arrays of L entries.  cbar = mean of conf over positions still masked after
+ * the step's commitment (masked_after != 0), summed in ascending position
+ * order; churn = fraction of those positions whose argmax differs from
+ * argmax_prev (0 on the first step: argmax_prev == NULL).  Empty set: 0, 0. */
+int davet_step_stats(int32_t L, const float* conf, const int32_t* argmax,
+                     const int32_t* argmax_prev, const uint8_t* masked_after,
+                     double* cbar, double* churn);
+
+/* ------------------------------------------------------------- schedule -- */
+
+/* The whole DAVET loop for a packed batch (Sec. 3.1 and Sec. 4; Fig. 2):
+ * davet_build_views once per sequence into view_bufs, then for t = 1..T:
+ * choose each sequence's level -- fixed_levels[s*T + t-1] when fixed_levels is
+ * given, else the policy pols[s] (Eqs. 7-9) from the signals of step t-1 --
+ * davet_denoise_step, davet_unmask with k.  In policy mode each step ends with
+ * one device-to-host copy of conf/argmax/flags and a stream synchronisation.
+ *   geoms: HOST [n_seqs] (d and dtype must match cfg)
+ *   visual: HOST [n_seqs] device pointers to each v
+ *   view_bufs: HOST [n_seqs*(K-1)] device pointers, pooled level l of
+ *              sequence s at view_bufs[s*(K-1) + l], sized by davet_view_sizes
+ *   prompt_ids/cu_prompt as in davet_denoise_step (cu_prompt on the HOST)
+ *   resp_ids / resp_masked: device, [n_seqs*L], in/out (normally all-masked
+ *              on entry)
+ *   pols: HOST [n_seqs] or NULL; fixed_levels: HOST [n_seqs*T] or NULL; exactly
+ *         one of the two must be given.
+ *   levels_out int32 / budgets_out double: HOST [n_seqs*T] or NULL
+ *         (budgets are NaN in fixed mode)
+ *   conf_trace float / argmax_trace int32: device [T, n_seqs*L] or NULL.
+ * Errors: as the calls it makes; EINVAL for a bad schedule argument. */
+int davet_run_schedule(const davet_model_cfg* cfg, const davet_weights* w,
+                       int32_t n_seqs, const davet_view_geom* geoms,
+                       const void* const* visual, void* const* view_bufs,
+                       const int32_t* prompt_ids, const int32_t* cu_prompt,
+                       int32_t L, int32_t T, int32_t k,
+                       const davet_policy* pols, const int32_t* fixed_levels,
+                       int32_t* resp_ids, uint8_t* resp_masked,
+                       int32_t* levels_out, double* budgets_out,
+                       float* conf_trace, int32_t* argmax_trace,
+                       void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------ profiling -- */
+
+/* Per-kernel-class timing with HIP events recorded around every launch on the
+ * launch stream (for the measurement harness).  davet_prof_enable(n) reserves
+ * event pairs for n launches (host-side and HIP event objects, created here,
+ * not in the steady state) and starts recording; davet_prof_enable(0) stops
+ * and releases them.  davet_prof_read synchronises on the recorded events and
+ * fills, per kernel class c < n_classes, the launch count and summed
+ * milliseconds; names via davet_prof_class_name.  Returns the number of
+ * classes, or a negative status. */
+int davet_prof_enable(int32_t max_launches);
+int davet_prof_reset(void);
+int davet_prof_read(int32_t n_classes, int64_t* counts /*host*/,
+                    double* total_ms /*host*/);
+const char* davet_prof_class_name(int32_t cls);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DAVET_H */

@@ -1,0 +1,150 @@
+// Internal helpers shared by the HIP sources of the DAVET library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string>
+
+#include "davet.h"
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+namespace davet {
+
+// ---- error reporting (host) ------------------------------------------------
+int set_error(int status, const std::string& msg);
+#define DAVET_CHECK_ARG(cond, status, msg) \
+  do { if (!(cond)) return ::davet::set_error((status), (msg)); } while (0)
+#define DAVET_HIP(call)                                                     \
+  do {                                                                      \
+    hipError_t e_ = (call);                                                 \
+    if (e_ != hipSuccess)                                                   \
+      return ::davet::set_error(DAVET_EHIP, std::string(#call) + ": " +    \
+                                hipGetErrorString(e_));                     \
+  } while (0)
+
+// ---- per-kernel-class launch timing (host) ---------------------------------
+enum KernelClass {
+  KC_VIEWS = 0, KC_VIEW_MAPS, KC_ASSEMBLE, KC_RMSNORM, KC_GEMM_QKV, KC_ROPE,
+  KC_ATTN, KC_GEMM_O, KC_GEMM_GATEUP, KC_GEMM_DOWN, KC_HEAD_PREP, KC_HEAD,
+  KC_HEAD_MERGE, KC_UNMASK, KC_GEMM_F32, KC_ATTN_F32, KC_MISC, KC_COUNT
+};
+const char* kernel_class_name(int c);
+// Brackets a launch with events when profiling is on; cheap no-op otherwise.
+struct ProfScope {
+  ProfScope(int cls, hipStream_t s);
+  ~ProfScope();
+  int slot;
+  hipStream_t stream;
+};
+
+// ---- bf16 helpers (device) -------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+// float32 -> bf16, round to nearest even (finite values; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+// float64 -> bf16 in a single rounding step (nearest, ties to even); normal
+// range values.  Keeps 7 of the 52 explicit mantissa bits of the double.
+__device__ __forceinline__ uint16_t f64_to_bf16(double x) {
+  uint64_t b = (uint64_t)__double_as_longlong(x);
+  uint64_t lsb = (b >> 45) & 1ull;
+  b = (b + ((1ull << 44) - 1ull) + lsb) & ~((1ull << 45) - 1ull);
+  float f = (float)__longlong_as_double((long long)b);   // exact
+  return (uint16_t)(__float_as_uint(f) >> 16);
+}
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float warp_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+inline size_t dtype_size(int dt) { return dt == DAVET_BF16 ? 2 : 4; }
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- kernel launchers (host, defined next to their kernels) ----------------
+// Views
+int launch_views(const davet_view_geom& g, const void* v, void* const* levels,
+                 hipStream_t s);
+int launch_view_maps(const davet_view_geom& g, int32_t* const* offs,
+                     int32_t* const* mem, hipStream_t s);
+
+// Packed-batch description passed by value to kernels.
+struct SeqPack {
+  int32_t n_seqs;
+  int32_t L;
+  int32_t total;                       // sum of N_s
+  int32_t row0[DAVET_MAX_SEQS + 1];    // first packed row of each sequence
+  int32_t nview[DAVET_MAX_SEQS];
+  int32_t pstart[DAVET_MAX_SEQS];      // offset into prompt_ids
+  int32_t plen[DAVET_MAX_SEQS];
+};
+struct ViewPtrs { const void* p[DAVET_MAX_SEQS]; };
+
+// Row kernels
+int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
+                         const void* embed, const int32_t* prompt_ids,
+                         const int32_t* resp_ids, const uint8_t* masked,
+                         int mask_id, int vocab, int d, const float* gain,
+                         float eps, float* X, void* A, hipStream_t s);
+int launch_rmsnorm(const float* X, int rows, int d, const float* gain,
+                   float eps, int dtype, void* A, hipStream_t s);
+int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
+                      hipStream_t s);
+int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
+                const SeqPack& sp, const float* cs, hipStream_t s);
+int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
+                     float* conf_out, int32_t* argmax_out, hipStream_t s);
+int launch_final_norm_gather(const float* X, const SeqPack& sp,
+                             const int32_t* list, int max_rows, int d,
+                             const float* gain, float eps, int dtype, void* Hm,
+                             hipStream_t s);
+int launch_head_merge(const int32_t* list, int max_rows, int n_slabs,
+                      const float* pmax, const float* psum, const int32_t* parg,
+                      float* conf_out, int32_t* argmax_out, hipStream_t s);
+int launch_head_reduce_f32(const float* logits, const int32_t* list,
+                           int max_rows, int vocab, int mask_id,
+                           float* conf_out, int32_t* argmax_out,
+                           float* logits_out, hipStream_t s);
+
+// GEMMs: C[M,N] = A[M,K] * B[N,K]^T
+enum Epilogue { EPI_STORE = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+int launch_gemm_bf16(int epi, const uint16_t* A, const uint16_t* B,
+                     const uint16_t* B2, void* C, int M, int N, int K,
+                     int ldc, int cls, hipStream_t s);
+int launch_head_bf16(const uint16_t* Hm, const uint16_t* W, const int32_t* list,
+                     int max_rows, int vocab, int d, int mask_id, float* pmax,
+                     float* psum, int32_t* parg, float* logits_out,
+                     hipStream_t s);
+int head_bf16_slabs(int vocab);
+int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
+                    float* C, int M, int N, int K, int ldc, int cls,
+                    const int32_t* m_count, hipStream_t s);
+
+// Attention over the packed batch: qkv [total, 3d] -> o [total, d]
+int launch_attention_bf16(const uint16_t* qkv, uint16_t* o, const SeqPack& sp,
+                          int n_heads, int head_dim, hipStream_t s);
+int launch_attention_f32(const float* qkv, float* o, const SeqPack& sp,
+                         int n_heads, int head_dim, hipStream_t s);
+
+int launch_unmask(int n_seqs, int L, int k, const float* conf,
+                  const int32_t* argmax, int32_t* ids, uint8_t* masked,
+                  int32_t* selected, hipStream_t s);
+
+}  // namespace davet

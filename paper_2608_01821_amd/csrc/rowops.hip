@@ -1,0 +1,426 @@
+// Row-wise kernels of the denoiser step: sequence assembly + embedding gather
+// fused with the first RMSNorm, RMSNorm, rotary embedding, masked-row
+// compaction, final norm of the masked rows, and the vocabulary-reduction
+// merge.  One workgroup (4 wavefronts) per row; reductions are wavefront
+// butterflies followed by a 4-entry LDS combine.
+
+#include "common.h"
+
+namespace davet {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = warp_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) t += red[i];
+  return t;
+}
+
+__device__ __forceinline__ int find_seq(const SeqPack& sp, int row) {
+  int s = 0;
+  while (s + 1 < sp.n_seqs && sp.row0[s + 1] <= row) ++s;
+  return s;
+}
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, int i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, int i) { return p[i]; }
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int i) {
+  return bf16_to_f32(p[i]);
+}
+template <typename T>
+__device__ __forceinline__ void store_elem(T* p, int i, float v);
+template <>
+__device__ __forceinline__ void store_elem<float>(float* p, int i, float v) { p[i] = v; }
+template <>
+__device__ __forceinline__ void store_elem<uint16_t>(uint16_t* p, int i, float v) {
+  p[i] = f32_to_bf16(v);
+}
+
+constexpr int kMaxPer = 32;   // d <= 8192 elements per row
+
+// X[row] = [view | E[prompt] | E[resp or mask]] row; A[row] = RMSNorm(X[row]).
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
+                     const int32_t* __restrict__ prompt_ids,
+                     const int32_t* __restrict__ resp_ids,
+                     const uint8_t* __restrict__ masked, int mask_id,
+                     int vocab, int d, const float* __restrict__ gain,
+                     float eps, float* __restrict__ X, T* __restrict__ A) {
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const int s = find_seq(sp, row);
+  const int j = row - sp.row0[s];
+  const T* src;
+  if (j < sp.nview[s]) {
+    src = reinterpret_cast<const T*>(vp.p[s]) + (size_t)j * d;
+  } else if (j < sp.nview[s] + sp.plen[s]) {
+    // ids outside [0, vocab) are clamped, never read out of bounds
+    const int id = min(max(prompt_ids[sp.pstart[s] + j - sp.nview[s]], 0),
+                       vocab - 1);
+    src = embed + (size_t)id * d;
+  } else {
+    const int i = j - sp.nview[s] - sp.plen[s];
+    const size_t q = (size_t)s * sp.L + i;
+    const int id = masked[q] ? mask_id : min(max(resp_ids[q], 0), vocab - 1);
+    src = embed + (size_t)id * d;
+  }
+  float x[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    x[n] = e < d ? load_elem(src, e) : 0.f;
+    ss += x[n] * x[n];
+  }
+  const float tot = block_sum(ss, red);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    if (e >= d) break;
+    X[(size_t)row * d + e] = x[n];
+    const float g = gain ? gain[e] : 1.0f;
+    store_elem(A + (size_t)row * d, e, x[n] * rstd * g);
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+rmsnorm_kernel(const float* __restrict__ X, int d,
+               const float* __restrict__ gain, float eps, T* __restrict__ A) {
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const float* x = X + (size_t)row * d;
+  float v[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    v[n] = e < d ? x[e] : 0.f;
+    ss += v[n] * v[n];
+  }
+  const float tot = block_sum(ss, red);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    if (e >= d) break;
+    const float g = gain ? gain[e] : 1.0f;
+    store_elem(A + (size_t)row * d, e, v[n] * rstd * g);
+  }
+}
+
+// cos/sin of pos * theta^(-2i/D), evaluated in float64 and rounded once.
+__global__ void rope_table_kernel(int max_pos, int head_dim, double theta,
+                                  float2* __restrict__ cs) {
+  const int half = head_dim / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= max_pos * half) return;
+  const int pos = idx / half, i = idx % half;
+  const double inv = pow(theta, -(2.0 * i) / (double)head_dim);
+  const double a = (double)pos * inv;
+  cs[idx] = make_float2((float)cos(a), (float)sin(a));
+}
+
+// In-place rotary embedding of the query and key parts of qkv [rows, 3d]:
+// dim i pairs with dim i + D/2 inside each head (rotate-half form).
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
+            const float2* __restrict__ cs) {
+  const int row = blockIdx.x;
+  const int s = find_seq(sp, row);
+  const int pos = row - sp.row0[s];
+  const int d = n_heads * head_dim;
+  const int half = head_dim / 2;
+  T* base = qkv + (size_t)row * 3 * d;
+  // 2 * n_heads * half pairs: queries then keys
+  for (int p = threadIdx.x; p < 2 * n_heads * half; p += kThreads) {
+    const int which = p / (n_heads * half);
+    const int h = (p / half) % n_heads;
+    const int i = p % half;
+    T* x = base + which * d + h * head_dim;
+    const float2 c = cs[(size_t)pos * half + i];
+    const float a = load_elem(x, i), b = load_elem(x, i + half);
+    store_elem(x, i, a * c.x - b * c.y);
+    store_elem(x, i + half, b * c.x + a * c.y);
+  }
+}
+
+// Single workgroup: ordered list of masked response positions (global index
+// s*L + i) with the count in list[0]; committed positions get conf = -inf and
+// argmax = -1.
+__global__ void __launch_bounds__(kThreads)
+head_prep_kernel(int total, const uint8_t* __restrict__ masked,
+                 int32_t* __restrict__ list, float* __restrict__ conf_out,
+                 int32_t* __restrict__ argmax_out) {
+  __shared__ int part[kThreads];
+  const int per = (total + kThreads - 1) / kThreads;
+  const int lo = threadIdx.x * per;
+  const int hi = min(total, lo + per);
+  int c = 0;
+  for (int i = lo; i < hi; ++i) c += masked[i] != 0;
+  part[threadIdx.x] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int t = 0; t < kThreads; ++t) {
+      const int v = part[t];
+      part[t] = run;
+      run += v;
+    }
+    list[0] = run;
+  }
+  __syncthreads();
+  int o = part[threadIdx.x];
+  for (int i = lo; i < hi; ++i) {
+    if (masked[i]) {
+      list[1 + o++] = i;
+    } else {
+      conf_out[i] = -INFINITY;
+      argmax_out[i] = -1;
+    }
+  }
+}
+
+// Hm[j] = RMSNorm_final(X[packed row of masked position list[1+j]]).
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+final_norm_gather_kernel(const float* __restrict__ X, SeqPack sp,
+                         const int32_t* __restrict__ list, int d,
+                         const float* __restrict__ gain, float eps,
+                         T* __restrict__ Hm) {
+  __shared__ float red[kThreads / 64];
+  const int j = blockIdx.x;
+  if (j >= list[0]) return;
+  const int g = list[1 + j];
+  const int s = g / sp.L, i = g % sp.L;
+  const int row = sp.row0[s] + sp.nview[s] + sp.plen[s] + i;
+  const float* x = X + (size_t)row * d;
+  float v[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    v[n] = e < d ? x[e] : 0.f;
+    ss += v[n] * v[n];
+  }
+  const float tot = block_sum(ss, red);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    if (e >= d) break;
+    const float gg = gain ? gain[e] : 1.0f;
+    store_elem(Hm + (size_t)j * d, e, v[n] * rstd * gg);
+  }
+}
+
+// (max, first argmax, sum of exp(l - max)) partials over vocabulary slabs ->
+// argmax (lowest id: slabs are in id order) and confidence 1 / sum.
+__global__ void __launch_bounds__(kThreads)
+head_merge_kernel(const int32_t* __restrict__ list, int n_slabs,
+                  const float* __restrict__ pmax, const float* __restrict__ psum,
+                  const int32_t* __restrict__ parg, float* __restrict__ conf_out,
+                  int32_t* __restrict__ argmax_out) {
+  __shared__ float rm[kThreads / 64];
+  __shared__ int ra[kThreads / 64];
+  __shared__ float red[kThreads / 64];
+  const int j = blockIdx.x;
+  if (j >= list[0]) return;
+  const float* mx = pmax + (size_t)j * n_slabs;
+  const float* sm = psum + (size_t)j * n_slabs;
+  const int32_t* ag = parg + (size_t)j * n_slabs;
+  float m = -INFINITY;
+  int a = 0x7fffffff;
+  for (int t = threadIdx.x; t < n_slabs; t += kThreads) {
+    const float v = mx[t];
+    const int id = ag[t];
+    if (v > m || (v == m && id < a)) { m = v; a = id; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v = __shfl_xor(m, o, 64);
+    const int id = __shfl_xor(a, o, 64);
+    if (v > m || (v == m && id < a)) { m = v; a = id; }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { rm[w] = m; ra[w] = a; }
+  __syncthreads();
+  m = rm[0]; a = ra[0];
+  for (int i = 1; i < kThreads / 64; ++i)
+    if (rm[i] > m || (rm[i] == m && ra[i] < a)) { m = rm[i]; a = ra[i]; }
+  float s = 0.f;
+  for (int t = threadIdx.x; t < n_slabs; t += kThreads)
+    s += sm[t] * __expf(mx[t] - m);
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) {
+    const int g = list[1 + j];
+    conf_out[g] = 1.0f / s;
+    argmax_out[g] = a;
+  }
+}
+
+// Float32 path: per masked row, reduce a full logits row.
+__global__ void __launch_bounds__(kThreads)
+head_reduce_f32_kernel(const float* __restrict__ logits,
+                       const int32_t* __restrict__ list, int V, int mask_id,
+                       float* __restrict__ conf_out,
+                       int32_t* __restrict__ argmax_out,
+                       float* __restrict__ logits_out) {
+  __shared__ float rm[kThreads / 64];
+  __shared__ int ra[kThreads / 64];
+  __shared__ float red[kThreads / 64];
+  const int j = blockIdx.x;
+  if (j >= list[0]) return;
+  const int g = list[1 + j];
+  const float* lg = logits + (size_t)j * V;
+  float m = -INFINITY;
+  int a = 0x7fffffff;
+  for (int t = threadIdx.x; t < V; t += kThreads) {
+    const float v = lg[t];
+    if (logits_out) logits_out[(size_t)g * V + t] = v;
+    if (t == mask_id) continue;
+    if (v > m || (v == m && t < a)) { m = v; a = t; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v = __shfl_xor(m, o, 64);
+    const int id = __shfl_xor(a, o, 64);
+    if (v > m || (v == m && id < a)) { m = v; a = id; }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { rm[w] = m; ra[w] = a; }
+  __syncthreads();
+  m = rm[0]; a = ra[0];
+  for (int i = 1; i < kThreads / 64; ++i)
+    if (rm[i] > m || (rm[i] == m && ra[i] < a)) { m = rm[i]; a = ra[i]; }
+  float s = 0.f;
+  for (int t = threadIdx.x; t < V; t += kThreads)
+    if (t != mask_id) s += expf(lg[t] - m);
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) {
+    conf_out[g] = 1.0f / s;
+    argmax_out[g] = a;
+  }
+}
+
+}  // namespace
+
+int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
+                         const void* embed, const int32_t* prompt_ids,
+                         const int32_t* resp_ids, const uint8_t* masked,
+                         int mask_id, int vocab, int d, const float* gain,
+                         float eps, float* X, void* A, hipStream_t s) {
+  ProfScope ps(KC_ASSEMBLE, s);
+  if (dtype == DAVET_BF16)
+    hipLaunchKernelGGL(assemble_norm_kernel<uint16_t>, dim3(sp.total),
+                       dim3(kThreads), 0, s, sp, vp,
+                       (const uint16_t*)embed, prompt_ids, resp_ids, masked,
+                       mask_id, vocab, d, gain, eps, X, (uint16_t*)A);
+  else
+    hipLaunchKernelGGL(assemble_norm_kernel<float>, dim3(sp.total),
+                       dim3(kThreads), 0, s, sp, vp, (const float*)embed,
+                       prompt_ids, resp_ids, masked, mask_id, vocab, d, gain,
+                       eps, X, (float*)A);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_rmsnorm(const float* X, int rows, int d, const float* gain,
+                   float eps, int dtype, void* A, hipStream_t s) {
+  ProfScope ps(KC_RMSNORM, s);
+  if (dtype == DAVET_BF16)
+    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(rows), dim3(kThreads), 0,
+                       s, X, d, gain, eps, (uint16_t*)A);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(kThreads), 0, s,
+                       X, d, gain, eps, (float*)A);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
+                      hipStream_t s) {
+  ProfScope ps(KC_MISC, s);
+  const int n = max_pos * (head_dim / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s,
+                     max_pos, head_dim, (double)theta, (float2*)cs);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
+                const SeqPack& sp, const float* cs, hipStream_t s) {
+  ProfScope ps(KC_ROPE, s);
+  if (dtype == DAVET_BF16)
+    hipLaunchKernelGGL(rope_kernel<uint16_t>, dim3(rows), dim3(kThreads), 0, s,
+                       (uint16_t*)qkv, sp, n_heads, head_dim,
+                       (const float2*)cs);
+  else
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(rows), dim3(kThreads), 0, s,
+                       (float*)qkv, sp, n_heads, head_dim, (const float2*)cs);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
+                     float* conf_out, int32_t* argmax_out, hipStream_t s) {
+  ProfScope ps(KC_HEAD_PREP, s);
+  hipLaunchKernelGGL(head_prep_kernel, dim3(1), dim3(kThreads), 0, s,
+                     sp.n_seqs * sp.L, masked, list, conf_out, argmax_out);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_final_norm_gather(const float* X, const SeqPack& sp,
+                             const int32_t* list, int max_rows, int d,
+                             const float* gain, float eps, int dtype, void* Hm,
+                             hipStream_t s) {
+  ProfScope ps(KC_HEAD_PREP, s);
+  if (dtype == DAVET_BF16)
+    hipLaunchKernelGGL(final_norm_gather_kernel<uint16_t>, dim3(max_rows),
+                       dim3(kThreads), 0, s, X, sp, list, d, gain, eps,
+                       (uint16_t*)Hm);
+  else
+    hipLaunchKernelGGL(final_norm_gather_kernel<float>, dim3(max_rows),
+                       dim3(kThreads), 0, s, X, sp, list, d, gain, eps,
+                       (float*)Hm);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_head_merge(const int32_t* list, int max_rows, int n_slabs,
+                      const float* pmax, const float* psum, const int32_t* parg,
+                      float* conf_out, int32_t* argmax_out, hipStream_t s) {
+  ProfScope ps(KC_HEAD_MERGE, s);
+  hipLaunchKernelGGL(head_merge_kernel, dim3(max_rows), dim3(kThreads), 0, s,
+                     list, n_slabs, pmax, psum, parg, conf_out, argmax_out);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_head_reduce_f32(const float* logits, const int32_t* list,
+                           int max_rows, int vocab, int mask_id,
+                           float* conf_out, int32_t* argmax_out,
+                           float* logits_out, hipStream_t s) {
+  ProfScope ps(KC_HEAD_MERGE, s);
+  hipLaunchKernelGGL(head_reduce_f32_kernel, dim3(max_rows), dim3(kThreads), 0,
+                     s, logits, list, vocab, mask_id, conf_out, argmax_out,
+                     logits_out);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+}  // namespace davet

@@ -1,0 +1,152 @@
+// The DAVET loop (Sec. 3.1 with Sec. 4; the procedure of Fig. 2): views are
+// built once per sample, then every step picks each sample's level (a fixed
+// schedule, or the allocation policy from the previous step's signals), runs
+// the denoiser and commits.  Policy mode reads conf/argmax/flags back once per
+// step (the only device-to-host crossing) to form the risk signals.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <vector>
+
+#include "common.h"
+
+namespace davet {
+void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
+                      int64_t L, size_t* conf_off, size_t* argmax_off);
+}
+
+extern "C" int davet_run_schedule(
+    const davet_model_cfg* cfg, const davet_weights* w, int32_t n_seqs,
+    const davet_view_geom* geoms, const void* const* visual,
+    void* const* view_bufs, const int32_t* prompt_ids, const int32_t* cu_prompt,
+    int32_t L, int32_t T, int32_t k, const davet_policy* pols,
+    const int32_t* fixed_levels, int32_t* resp_ids, uint8_t* resp_masked,
+    int32_t* levels_out, double* budgets_out, float* conf_trace,
+    int32_t* argmax_trace, void* workspace, size_t ws_bytes,
+    hipStream_t stream) {
+  using namespace davet;
+  DAVET_CHECK_ARG(cfg && w && geoms && visual && cu_prompt && resp_ids &&
+                      resp_masked && workspace,
+                  DAVET_EINVAL, "davet_run_schedule: null argument");
+  DAVET_CHECK_ARG(n_seqs >= 1 && n_seqs <= DAVET_MAX_SEQS, DAVET_ESHAPE,
+                  "davet_run_schedule: n_seqs out of range");
+  DAVET_CHECK_ARG(T >= 1 && k >= 1, DAVET_EINVAL,
+                  "davet_run_schedule: T >= 1 and k >= 1 required");
+  DAVET_CHECK_ARG((pols == nullptr) != (fixed_levels == nullptr), DAVET_EINVAL,
+                  "davet_run_schedule: give exactly one of pols, fixed_levels");
+  DAVET_CHECK_ARG(L >= 1 && L <= DAVET_MAX_RESP, DAVET_ESHAPE,
+                  "davet_run_schedule: L out of range");
+  const int K = geoms[0].K;
+  DAVET_CHECK_ARG(K >= 1 && K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
+                  "davet_run_schedule: K out of range");
+  DAVET_CHECK_ARG(K == 1 || view_bufs, DAVET_EINVAL,
+                  "davet_run_schedule: view_bufs is null");
+
+  // views: level pointers and sizes per sequence
+  std::vector<const void*> lvl_ptr((size_t)n_seqs * K);
+  std::vector<int32_t> lvl_n((size_t)n_seqs * K);
+  int64_t max_tokens = 0;
+  for (int s = 0; s < n_seqs; ++s) {
+    const davet_view_geom& g = geoms[s];
+    DAVET_CHECK_ARG(g.K == K && g.d == cfg->d && g.dtype == cfg->dtype,
+                    DAVET_ESHAPE,
+                    "davet_run_schedule: geometry K/d/dtype must match cfg");
+    int rc = davet_view_sizes(&g, &lvl_n[(size_t)s * K]);
+    if (rc) return rc;
+    for (int l = 0; l < K; ++l)
+      lvl_ptr[(size_t)s * K + l] =
+          l == K - 1 ? visual[s] : view_bufs[(size_t)s * (K - 1) + l];
+    max_tokens += lvl_n[(size_t)s * K + K - 1] + (cu_prompt[s + 1] - cu_prompt[s]) + L;
+  }
+  if (fixed_levels)
+    for (int i = 0; i < n_seqs * T; ++i)
+      DAVET_CHECK_ARG(fixed_levels[i] >= 0 && fixed_levels[i] < K, DAVET_EINVAL,
+                      "davet_run_schedule: fixed level out of range");
+  size_t need = 0;
+  {
+    int rc = davet_workspace_bytes(cfg, (int32_t)max_tokens, n_seqs, L, &need);
+    if (rc) return rc;
+  }
+  DAVET_CHECK_ARG(ws_bytes >= need, DAVET_ENOMEM,
+                  "davet_run_schedule: workspace smaller than the full-view size");
+  size_t conf_off = 0, am_off = 0;
+  schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off);
+  char* ws = static_cast<char*>(workspace);
+
+  // a1: evidence views, once per sample
+  for (int s = 0; s < n_seqs; ++s) {
+    std::vector<void*> lv(K, nullptr);
+    for (int l = 0; l < K - 1; ++l) lv[l] = view_bufs[(size_t)s * (K - 1) + l];
+    int rc = davet_build_views(&geoms[s], visual[s], lv.data(), nullptr,
+                               nullptr, stream);
+    if (rc) return rc;
+  }
+
+  // policy state
+  std::vector<double> lower, upper;
+  if (pols) {
+    lower.resize((size_t)n_seqs * T);
+    upper.resize((size_t)n_seqs * T);
+    for (int s = 0; s < n_seqs; ++s) {
+      DAVET_CHECK_ARG(pols[s].K == K, DAVET_EINVAL,
+                      "davet_run_schedule: policy K must match the views");
+      int rc = davet_policy_envelope(&pols[s], T, &lower[(size_t)s * T],
+                                     &upper[(size_t)s * T]);
+      if (rc) return rc;
+    }
+  }
+  std::vector<double> cbar(n_seqs, 0.0), churn(n_seqs, 0.0);
+  std::vector<float> conf_h((size_t)n_seqs * L);
+  std::vector<int32_t> am_h((size_t)n_seqs * L), am_prev((size_t)n_seqs * L);
+  std::vector<uint8_t> mask_h((size_t)n_seqs * L);
+  std::vector<const void*> vptr(n_seqs);
+  std::vector<int32_t> nview(n_seqs);
+
+  for (int t = 1; t <= T; ++t) {
+    for (int s = 0; s < n_seqs; ++s) {
+      int lv;
+      double b = NAN;
+      if (pols) {
+        int rc = davet_policy_step(&pols[s], t, T, &lower[(size_t)s * T],
+                                   &upper[(size_t)s * T], cbar[s], churn[s],
+                                   &b, &lv, nullptr);
+        if (rc) return rc;
+      } else {
+        lv = fixed_levels[(size_t)s * T + (t - 1)];
+      }
+      if (levels_out) levels_out[(size_t)s * T + (t - 1)] = lv;
+      if (budgets_out) budgets_out[(size_t)s * T + (t - 1)] = b;
+      vptr[s] = lvl_ptr[(size_t)s * K + lv];
+      nview[s] = lvl_n[(size_t)s * K + lv];
+    }
+    float* conf = conf_trace ? conf_trace + (size_t)(t - 1) * n_seqs * L
+                             : reinterpret_cast<float*>(ws + conf_off);
+    int32_t* am = argmax_trace ? argmax_trace + (size_t)(t - 1) * n_seqs * L
+                               : reinterpret_cast<int32_t*>(ws + am_off);
+    int rc = davet_denoise_step(cfg, w, n_seqs, vptr.data(), nview.data(),
+                                prompt_ids, cu_prompt, resp_ids, resp_masked, L,
+                                conf, am, nullptr, workspace, ws_bytes, stream);
+    if (rc) return rc;
+    rc = davet_unmask(n_seqs, L, k, conf, am, resp_ids, resp_masked, nullptr,
+                      stream);
+    if (rc) return rc;
+    if (pols && t < T) {
+      // signals of step t for the risk of step t+1 (Sec. 4.2)
+      const size_t n = (size_t)n_seqs * L;
+      DAVET_HIP(hipMemcpyAsync(conf_h.data(), conf, n * 4, hipMemcpyDeviceToHost, stream));
+      DAVET_HIP(hipMemcpyAsync(am_h.data(), am, n * 4, hipMemcpyDeviceToHost, stream));
+      DAVET_HIP(hipMemcpyAsync(mask_h.data(), resp_masked, n, hipMemcpyDeviceToHost, stream));
+      DAVET_HIP(hipStreamSynchronize(stream));
+      for (int s = 0; s < n_seqs; ++s) {
+        const size_t o = (size_t)s * L;
+        rc = davet_step_stats(L, &conf_h[o], &am_h[o],
+                              t == 1 ? nullptr : &am_prev[o], &mask_h[o],
+                              &cbar[s], &churn[s]);
+        if (rc) return rc;
+      }
+      am_prev.swap(am_h);
+    }
+  }
+  return DAVET_OK;
+}

@@ -1,0 +1,271 @@
+// One denoising step (Sec. 3.1, Eq. 1) over a packed batch, and the workspace
+// layout it uses.  The host side only validates, packs the per-sequence table
+// and enqueues kernels; every arithmetic step runs on the GPU.
+//
+// Layer schedule (pre-norm, n_layers times):
+//   A = RMSNorm(X)                 (fused into the assembly for layer 0, and
+//                                   into the previous layer's tail otherwise)
+//   QKV = A Wqkv^T                 GEMM, bf16 out
+//   rotary embedding on Q, K       in place
+//   O = attention(Q, K, V)         non-causal, per sequence
+//   X += O Wo^T                    GEMM, fp32 residual epilogue
+//   A = RMSNorm(X)
+//   H = silu(A Wg^T) * (A Wu^T)    dual GEMM, SwiGLU epilogue
+//   X += H Wd^T                    GEMM, fp32 residual epilogue
+// then the final norm of the masked response rows, the vocabulary GEMM with
+// the fused (max, argmax, sum-exp) reduction, and the merge across slabs.
+
+#include <algorithm>
+#include <vector>
+
+#include "common.h"
+
+namespace davet {
+
+struct Layout {
+  size_t conf, argmax;                 // run_schedule scratch
+  size_t X, A, QKV, O, H, rope, list, Hm, pmax, psum, parg, logits;
+  size_t total;
+};
+
+static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
+                          int64_t seqs, int64_t L) {
+  const size_t es = dtype_size(c.dtype);
+  const int64_t rows = seqs * L;
+  const int64_t slabs = head_bf16_slabs(c.vocab);
+  Layout o{};
+  size_t p = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = p;
+    p = align_up(p + bytes, 256);
+    return at;
+  };
+  o.conf = take(rows * 4);
+  o.argmax = take(rows * 4);
+  o.X = take((size_t)tokens * c.d * 4);
+  o.A = take((size_t)tokens * c.d * es);
+  o.QKV = take((size_t)tokens * 3 * c.d * es);
+  o.O = take((size_t)tokens * c.d * es);
+  o.H = take((size_t)tokens * c.ffn * es);
+  o.rope = take((size_t)tokens * (c.head_dim / 2) * 8);
+  o.list = take((size_t)(rows + 1) * 4);
+  o.Hm = take((size_t)rows * c.d * es);
+  if (c.dtype == DAVET_BF16) {
+    o.pmax = take((size_t)rows * slabs * 4);
+    o.psum = take((size_t)rows * slabs * 4);
+    o.parg = take((size_t)rows * slabs * 4);
+    o.logits = 0;
+  } else {
+    o.logits = take((size_t)rows * c.vocab * 4);
+  }
+  o.total = p;
+  return o;
+}
+
+static int check_cfg(const davet_model_cfg* c) {
+  DAVET_CHECK_ARG(c, DAVET_EINVAL, "model cfg is null");
+  DAVET_CHECK_ARG(c->dtype == DAVET_F32 || c->dtype == DAVET_BF16, DAVET_EDTYPE,
+                  "cfg.dtype must be DAVET_F32 or DAVET_BF16");
+  DAVET_CHECK_ARG(c->n_layers >= 0 && c->n_heads >= 1, DAVET_ESHAPE,
+                  "cfg: n_layers >= 0 and n_heads >= 1 required");
+  DAVET_CHECK_ARG(c->head_dim == 64 || c->head_dim == 128, DAVET_ESHAPE,
+                  "cfg.head_dim must be 64 or 128");
+  DAVET_CHECK_ARG(c->d == c->n_heads * c->head_dim, DAVET_ESHAPE,
+                  "cfg.d must equal n_heads * head_dim");
+  DAVET_CHECK_ARG(c->d <= 8192 && c->ffn >= 1, DAVET_ESHAPE,
+                  "cfg.d must be <= 8192, ffn >= 1");
+  DAVET_CHECK_ARG(c->vocab >= 2 && c->mask_id >= 0 && c->mask_id < c->vocab,
+                  DAVET_ESHAPE, "cfg: vocab >= 2 and 0 <= mask_id < vocab");
+  DAVET_CHECK_ARG(c->rms_eps >= 0.f && c->rope_theta > 0.f, DAVET_EINVAL,
+                  "cfg: rms_eps >= 0 and rope_theta > 0 required");
+  if (c->dtype == DAVET_BF16) {
+    DAVET_CHECK_ARG(c->head_dim == 128, DAVET_ESHAPE,
+                    "bf16 path: head_dim must be 128");
+    DAVET_CHECK_ARG(c->d % 128 == 0 && c->ffn % 64 == 0 && (3 * c->d) % 128 == 0,
+                    DAVET_ESHAPE, "bf16 path: d % 128 == 0 and ffn % 64 == 0");
+  }
+  return DAVET_OK;
+}
+
+int workspace_layout_bytes(const davet_model_cfg* c, int64_t tokens,
+                           int64_t seqs, int64_t L, size_t* out) {
+  *out = make_layout(*c, tokens, seqs, L).total;
+  return DAVET_OK;
+}
+
+// Used by run_schedule to reach its scratch region.
+void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
+                      int64_t L, size_t* conf_off, size_t* argmax_off) {
+  const Layout o = make_layout(*c, tokens, seqs, L);
+  *conf_off = o.conf;
+  *argmax_off = o.argmax;
+}
+
+}  // namespace davet
+
+extern "C" int davet_workspace_bytes(const davet_model_cfg* cfg,
+                                     int32_t max_tokens, int32_t max_seqs,
+                                     int32_t L, size_t* bytes) {
+  using namespace davet;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  DAVET_CHECK_ARG(bytes, DAVET_EINVAL, "davet_workspace_bytes: bytes is null");
+  DAVET_CHECK_ARG(max_tokens >= 1 && max_seqs >= 1 &&
+                      max_seqs <= DAVET_MAX_SEQS && L >= 1 && L <= DAVET_MAX_RESP,
+                  DAVET_ESHAPE, "davet_workspace_bytes: sizes out of range");
+  return workspace_layout_bytes(cfg, max_tokens, max_seqs, L, bytes);
+}
+
+extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
+                                  const davet_weights* w, int32_t n_seqs,
+                                  const void* const* view_ptrs,
+                                  const int32_t* n_view,
+                                  const int32_t* prompt_ids,
+                                  const int32_t* cu_prompt,
+                                  const int32_t* resp_ids,
+                                  const uint8_t* resp_masked, int32_t L,
+                                  float* conf_out, int32_t* argmax_out,
+                                  float* logits_out, void* workspace,
+                                  size_t ws_bytes, hipStream_t stream) {
+  using namespace davet;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  const davet_model_cfg& c = *cfg;
+  DAVET_CHECK_ARG(w && w->embed && w->head, DAVET_EINVAL,
+                  "davet_denoise_step: null weights");
+  DAVET_CHECK_ARG(c.n_layers == 0 || w->layers, DAVET_EINVAL,
+                  "davet_denoise_step: null layer table");
+  for (int l = 0; l < c.n_layers; ++l) {
+    const davet_layer_weights& lw = w->layers[l];
+    DAVET_CHECK_ARG(lw.wqkv && lw.wo && lw.wg && lw.wu && lw.wd, DAVET_EINVAL,
+                    "davet_denoise_step: null layer weight");
+  }
+  DAVET_CHECK_ARG(n_seqs >= 1 && n_seqs <= DAVET_MAX_SEQS, DAVET_ESHAPE,
+                  "davet_denoise_step: n_seqs out of range [1, 64]");
+  DAVET_CHECK_ARG(L >= 1 && L <= DAVET_MAX_RESP, DAVET_ESHAPE,
+                  "davet_denoise_step: L out of range [1, 1024]");
+  DAVET_CHECK_ARG(view_ptrs && n_view && cu_prompt && resp_ids && resp_masked &&
+                      conf_out && argmax_out && workspace,
+                  DAVET_EINVAL, "davet_denoise_step: null pointer");
+  DAVET_CHECK_ARG(cu_prompt[0] == 0, DAVET_ESHAPE,
+                  "davet_denoise_step: cu_prompt[0] must be 0");
+  DAVET_CHECK_ARG(((uintptr_t)workspace & 255) == 0, DAVET_ENOMEM,
+                  "davet_denoise_step: workspace must be 256-byte aligned");
+
+  SeqPack sp{};
+  ViewPtrs vp{};
+  sp.n_seqs = n_seqs;
+  sp.L = L;
+  int64_t total = 0;
+  int max_n = 0;
+  for (int s = 0; s < n_seqs; ++s) {
+    DAVET_CHECK_ARG(n_view[s] >= 0, DAVET_ESHAPE,
+                    "davet_denoise_step: negative view length");
+    DAVET_CHECK_ARG(n_view[s] == 0 || view_ptrs[s], DAVET_EINVAL,
+                    "davet_denoise_step: null view pointer");
+    const int plen = cu_prompt[s + 1] - cu_prompt[s];
+    DAVET_CHECK_ARG(plen >= 0, DAVET_ESHAPE,
+                    "davet_denoise_step: cu_prompt must be non-decreasing");
+    DAVET_CHECK_ARG(plen == 0 || prompt_ids, DAVET_EINVAL,
+                    "davet_denoise_step: null prompt_ids");
+    const int64_t n = (int64_t)n_view[s] + plen + L;
+    sp.row0[s] = (int32_t)total;
+    sp.nview[s] = n_view[s];
+    sp.pstart[s] = cu_prompt[s];
+    sp.plen[s] = plen;
+    vp.p[s] = view_ptrs[s];
+    total += n;
+    max_n = std::max<int64_t>(max_n, n);
+    DAVET_CHECK_ARG(total < (1ll << 30), DAVET_ESHAPE,
+                    "davet_denoise_step: too many tokens");
+  }
+  sp.row0[n_seqs] = (int32_t)total;
+  sp.total = (int32_t)total;
+  const Layout lay = make_layout(c, total, n_seqs, L);
+  DAVET_CHECK_ARG(ws_bytes >= lay.total, DAVET_ENOMEM,
+                  "davet_denoise_step: workspace too small (" +
+                      std::to_string(ws_bytes) + " < " +
+                      std::to_string(lay.total) + " bytes)");
+
+  char* ws = static_cast<char*>(workspace);
+  float* X = reinterpret_cast<float*>(ws + lay.X);
+  void* A = ws + lay.A;
+  void* QKV = ws + lay.QKV;
+  void* O = ws + lay.O;
+  void* H = ws + lay.H;
+  float* rope = reinterpret_cast<float*>(ws + lay.rope);
+  int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
+  void* Hm = ws + lay.Hm;
+  const int rows = n_seqs * L;
+  const bool bf = c.dtype == DAVET_BF16;
+  const int d = c.d, F = c.ffn;
+  hipStream_t s = stream;
+
+#define RUN(x) do { int rc_ = (x); if (rc_) return rc_; } while (0)
+  RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta, rope, s));
+  RUN(launch_head_prep(sp, resp_masked, list, conf_out, argmax_out, s));
+  const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
+  RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,
+                           resp_masked, c.mask_id, c.vocab, d, g0, c.rms_eps, X, A,
+                           s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const davet_layer_weights& lw = w->layers[l];
+    if (l > 0) RUN(launch_rmsnorm(X, sp.total, d, lw.attn_norm, c.rms_eps,
+                                  c.dtype, A, s));
+    if (bf) {
+      RUN(launch_gemm_bf16(EPI_STORE, (const uint16_t*)A,
+                           (const uint16_t*)lw.wqkv, nullptr, QKV, sp.total,
+                           3 * d, d, 3 * d, KC_GEMM_QKV, s));
+      RUN(launch_rope(QKV, sp.total, c.n_heads, c.head_dim, c.dtype, sp, rope, s));
+      RUN(launch_attention_bf16((const uint16_t*)QKV, (uint16_t*)O, sp,
+                                c.n_heads, c.head_dim, s));
+      RUN(launch_gemm_bf16(EPI_ADD_F32, (const uint16_t*)O,
+                           (const uint16_t*)lw.wo, nullptr, X, sp.total, d, d,
+                           d, KC_GEMM_O, s));
+      RUN(launch_rmsnorm(X, sp.total, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
+      RUN(launch_gemm_bf16(EPI_SWIGLU, (const uint16_t*)A,
+                           (const uint16_t*)lw.wg, (const uint16_t*)lw.wu, H,
+                           sp.total, 2 * F, d, F, KC_GEMM_GATEUP, s));
+      RUN(launch_gemm_bf16(EPI_ADD_F32, (const uint16_t*)H,
+                           (const uint16_t*)lw.wd, nullptr, X, sp.total, d, F,
+                           d, KC_GEMM_DOWN, s));
+    } else {
+      RUN(launch_gemm_f32(EPI_STORE, (const float*)A, (const float*)lw.wqkv,
+                          nullptr, (float*)QKV, sp.total, 3 * d, d, 3 * d,
+                          KC_GEMM_F32, nullptr, s));
+      RUN(launch_rope(QKV, sp.total, c.n_heads, c.head_dim, c.dtype, sp, rope, s));
+      RUN(launch_attention_f32((const float*)QKV, (float*)O, sp, c.n_heads,
+                               c.head_dim, s));
+      RUN(launch_gemm_f32(EPI_ADD_F32, (const float*)O, (const float*)lw.wo,
+                          nullptr, X, sp.total, d, d, d, KC_GEMM_F32, nullptr, s));
+      RUN(launch_rmsnorm(X, sp.total, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
+      RUN(launch_gemm_f32(EPI_SWIGLU, (const float*)A, (const float*)lw.wg,
+                          (const float*)lw.wu, (float*)H, sp.total, F, d, F,
+                          KC_GEMM_F32, nullptr, s));
+      RUN(launch_gemm_f32(EPI_ADD_F32, (const float*)H, (const float*)lw.wd,
+                          nullptr, X, sp.total, d, F, d, KC_GEMM_F32, nullptr, s));
+    }
+  }
+  RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
+                               c.dtype, Hm, s));
+  if (bf) {
+    const int slabs = head_bf16_slabs(c.vocab);
+    float* pmax = reinterpret_cast<float*>(ws + lay.pmax);
+    float* psum = reinterpret_cast<float*>(ws + lay.psum);
+    int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);
+    RUN(launch_head_bf16((const uint16_t*)Hm, (const uint16_t*)w->head, list,
+                         rows, c.vocab, d, c.mask_id, pmax, psum, parg,
+                         logits_out, s));
+    RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
+                          argmax_out, s));
+  } else {
+    float* logits = reinterpret_cast<float*>(ws + lay.logits);
+    RUN(launch_gemm_f32(EPI_STORE, (const float*)Hm, (const float*)w->head,
+                        nullptr, logits, rows, c.vocab, d, c.vocab, KC_HEAD,
+                        list, s));
+    RUN(launch_head_reduce_f32(logits, list, rows, c.vocab, c.mask_id,
+                               conf_out, argmax_out, logits_out, s));
+  }
+#undef RUN
+  return DAVET_OK;
+}

@@ -9,7 +9,7 @@ Rounding to bfloat16 (round-to-nearest-even) is part of input preparation:
 the bf16 configurations hand both sides the same bf16-representable values.
 """
 
-from .configs import CONFIGS, Config, get_config  # noqa: F401
+from .configs import CONFIGS, TEST_CONFIGS, Config, get_config, get_any_config  # noqa: F401,E501
 from .gen import (  # noqa: F401
     bf16_bits_to_f32,
     f32_to_bf16_bits,

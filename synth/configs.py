@@ -98,3 +98,27 @@ CONFIGS = {
 
 def get_config(cid: int) -> Config:
     return CONFIGS[int(cid)]
+
+
+# Small shapes for parity tests: several tiles with ragged tails everywhere
+# (pooling edges, GEMM rows, attention keys, vocabulary slabs).
+TEST_CONFIGS = {
+    11: Config(cid=11, name="mini-bf16", dtype="bf16", n_layers=2, d=256,
+               n_heads=2, head_dim=128, ffn=512, vocab=1000, grid=7,
+               n_crops=2, prompt_len=13, resp_len=37, steps=6, k=7,
+               schedule="fixed", fixed_levels=(2, 0, 1, 1, 0, 2)),
+    12: Config(cid=12, name="mini-bf16-ragged", dtype="bf16", n_layers=1,
+               d=256, n_heads=2, head_dim=128, ffn=512, vocab=1000, grid=9,
+               n_crops=0, prompt_len=0, resp_len=24, steps=4, k=6,
+               n_seqs=5, schedule="policy", crops_range=(1, 3),
+               prompt_range=(3, 40)),
+    13: Config(cid=13, name="mini-f32-ragged", dtype="f32", n_layers=2,
+               d=128, n_heads=2, head_dim=64, ffn=256, vocab=300, grid=5,
+               n_crops=0, prompt_len=0, resp_len=20, steps=5, k=4,
+               n_seqs=3, schedule="policy", crops_range=(1, 2),
+               prompt_range=(2, 9)),
+}
+
+
+def get_any_config(cid: int) -> Config:
+    return CONFIGS[int(cid)] if int(cid) in CONFIGS else TEST_CONFIGS[int(cid)]

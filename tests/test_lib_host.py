@@ -1,0 +1,128 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every entry point include/davet.h declares, rejects bad arguments before
+enqueueing anything, and its host policy matches the oracle bit for bit."""
+
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import paper_2608_01821_amd as dv
+from oracle import policy as opol
+from oracle import stats as ostats
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include",
+                      "davet.h")
+
+
+def test_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(davet_[a-z_0-9]+)\s*\(", text))
+    assert declared, "no declarations found"
+    lib = dv.raw()
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared <= set(dv.EXPORTED)
+    assert "gfx950" in dv.davet_version()
+
+
+def test_demand_prior_table(golden_dir):
+    import json
+    g = json.load(open(os.path.join(golden_dir, "table_a_demand_prior.json")))
+    assert [dv.davet_demand_prior(i) for i in range(5)] == g["demand"]
+    assert dv.davet_demand_prior(5) < 0 and dv.davet_demand_prior(-1) < 0
+
+
+def _pol(B, rho, alpha, demand, early, K=3):
+    return dv.Policy(B, rho, alpha, demand, 1 if early else 0, K)
+
+
+@settings(max_examples=300, deadline=None)
+@given(T=st.integers(1, 160), early=st.booleans(), B=st.floats(0.0, 1.2),
+       rho=st.floats(0.0, 1.0), d=st.floats(0.0, 1.0),
+       alpha=st.floats(0.0, 1.0), K=st.integers(1, 4), data=st.data())
+def test_policy_bit_exact_vs_oracle(T, early, B, rho, d, alpha, K, data):
+    pol = _pol(B, rho, alpha, d, early, K)
+    lo, up = dv.davet_policy_envelope(pol, T)
+    olo, oup = opol.envelope(T, early, B, rho, d)
+    assert lo == olo and up == oup          # bitwise, element by element
+    cb = data.draw(st.floats(0.0, 1.0))
+    ch = data.draw(st.floats(0.0, 1.0))
+    for t in range(1, T + 1):
+        b, lv, r = dv.davet_policy_step(pol, t, T, lo, up, cb, ch)
+        ob, olv, orr = opol.step(t, olo, oup, alpha, cb, ch, K)
+        assert (b, lv, r) == (ob, olv, orr)
+
+
+def test_policy_paper_defaults_closed_form():
+    # Sec. 5.1 defaults; hand-derived levels (see the oracle's pins)
+    pol = _pol(0.75, 0.20, 1.0, 1.0, True)
+    lo, up = dv.davet_policy_envelope(pol, 16)
+    assert up == [min(1.0, (33 - 2 * t) / 16) for t in range(1, 17)]
+    lv = [dv.davet_policy_step(pol, t, 16, lo, up, 0.0, 0.0)[1]
+          for t in range(1, 17)]
+    assert "".join(map(str, lv)) == "2222222222211000"   # r = 1
+    lv0 = [dv.davet_policy_step(pol, t, 16, lo, up, 1.0, 0.0)[1]
+           for t in range(2, 17)]
+    assert "".join(map(str, lv0)) == "222222111110000"    # r = 0 after t = 1
+
+
+@settings(max_examples=200, deadline=None)
+@given(data=st.data(), L=st.integers(0, 64), first=st.booleans())
+def test_step_stats_bit_exact_vs_oracle(data, L, first):
+    rng = np.random.default_rng(data.draw(st.integers(0, 2 ** 31)))
+    conf = rng.random(L).astype(np.float32)
+    am = rng.integers(0, 5, L).astype(np.int32)
+    prev = rng.integers(0, 5, L).astype(np.int32)
+    m = rng.integers(0, 2, L).astype(np.uint8)
+    cb, ch = dv.davet_step_stats(conf, am, None if first else prev, m)
+    assert cb == ostats.mean_conf(conf, m)
+    assert ch == ostats.churn(am, prev, m, first)
+
+
+def _expect(status, fn, *a, **k):
+    with pytest.raises(dv.DavetError) as e:
+        fn(*a, **k)
+    assert e.value.status == status
+
+
+def test_argument_validation_without_gpu():
+    # every check below fails before any HIP call is made
+    g = dv.ViewGeom(1, 12, 256, 3, dv.DAVET_F32)
+    assert dv.davet_view_sizes(g) == [9, 36, 144]
+    assert dv.davet_view_sizes(dv.ViewGeom(5, 27, 4096, 3, 1)) == \
+        [245, 980, 3645]
+    _expect(-2, dv.davet_view_sizes, dv.ViewGeom(1, 12, 256, 5, 0))
+    _expect(-2, dv.davet_view_sizes, dv.ViewGeom(0, 12, 256, 3, 0))
+    lib = dv.raw()
+    import ctypes as C
+    assert lib.davet_build_views(C.byref(g), None, None, None, None, None) == -1
+    bad = dv.ViewGeom(1, 12, 250, 3, dv.DAVET_F32)
+    assert lib.davet_build_views(C.byref(bad), C.c_void_p(16), None, None,
+                                 None, None) == -2
+    assert lib.davet_unmask(1, 32, 0, C.c_void_p(16), C.c_void_p(16),
+                            C.c_void_p(16), C.c_void_p(16), None, None) == -1
+    assert lib.davet_unmask(1, 2000, 2, C.c_void_p(16), C.c_void_p(16),
+                            C.c_void_p(16), C.c_void_p(16), None, None) == -2
+    cfg = dv.ModelCfg(1, 4096, 32, 128, 12288, 126464, 126463, 1e-5, 1e4,
+                      dv.DAVET_BF16)
+    assert dv.davet_workspace_bytes(cfg, 1000, 1, 128) > 0
+    badcfg = dv.ModelCfg(1, 4096, 32, 96, 12288, 126464, 126463, 1e-5, 1e4,
+                         dv.DAVET_BF16)
+    _expect(-2, dv.davet_workspace_bytes, badcfg, 1000, 1, 128)
+    badcfg = dv.ModelCfg(1, 4096, 32, 128, 12288, 126464, 126464, 1e-5, 1e4,
+                         dv.DAVET_BF16)
+    _expect(-2, dv.davet_workspace_bytes, badcfg, 1000, 1, 128)
+    badcfg = dv.ModelCfg(1, 4096, 32, 128, 12288, 126464, 5, 1e-5, 1e4, 7)
+    _expect(-3, dv.davet_workspace_bytes, badcfg, 1000, 1, 128)
+    _expect(-2, dv.davet_workspace_bytes, cfg, 1000, 65, 128)
+    pol = _pol(0.75, 0.2, 1.0, 1.0, True)
+    _expect(-1, dv.davet_policy_envelope, pol, 0)
+    _expect(-1, dv.davet_policy_envelope, _pol(math.nan, 0.2, 1, 1, True), 4)
+    lo, up = dv.davet_policy_envelope(pol, 4)
+    _expect(-1, dv.davet_policy_step, pol, 5, 4, lo, up, 0.0, 0.0)
+    _expect(-1, dv.davet_policy_step, _pol(0.75, 0.2, 1, 1, True, 9), 1, 4,
+            lo, up, 0.0, 0.0)
