@@ -1,0 +1,347 @@
+#!/usr/bin/env python3
+"""Throughput of the DAVET hot path on one MI355X.
+
+One bench "step" is one full pass of the hot path over one batch: the
+evidence views are built once, then the whole T-step denoising loop runs
+(level choice, assembly, layer stack, vocabulary head, commitment) through
+``davet_run_schedule``.  ``value`` is denoising steps per second (T times the
+loops timed, over the wall time of the timed region), with every input
+already resident in HBM.
+
+Defaults: the one-layer 8B-shaped bf16 workload (d=4096, 32 heads x 128,
+SwiGLU 12288, vocab 126464; one 27x27 crop = 729 visual tokens, pyramid
+729/196/49; prompt 32, response 128; 64 steps committing 2 per step; high
+view for the first quarter of the steps, coarse after).  ``--config`` picks
+another workload (1 tiny fp32, 3 five crops, 4 32-layer stack, 5 ragged
+batch of 16).
+
+Also reported, in the same JSON line:
+  roofline      the dominant kernel class: algorithmic work per launch
+                divided by its mean launch time, timed with HIP events around
+                every launch on the library's stream inside the timed region
+  cpu_baseline  the CPU oracle timed on this host on a bounded sample (one
+                oracle step per view level the schedule uses, extrapolated to
+                the schedule)
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
+PEAK_FP32_TFLOPS = 157.3       # fp32 vector peak
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5,
+                    help="timed passes of the full T-step loop")
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="skip the per-launch HIP events")
+    ap.add_argument("--cpu-layers", type=int, default=1,
+                    help="layers the CPU oracle runs (extrapolated beyond)")
+    return ap.parse_args()
+
+
+def setup(cfg):
+    import numpy as np
+    import torch
+
+    import paper_2608_01821_amd as dv
+    import synth
+
+    t0 = time.time()
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)
+                                if bits.dtype == np.uint16 else bits).cuda()
+
+    bf = cfg.dtype == "bf16"
+    layers = []
+    for li in range(cfg.n_layers):
+        lw = synth.gen_layer_weights(cfg, li, as_bits=bf)
+        layers.append({k: dev(v) for k, v in lw.items()})
+        del lw
+    embed = dev(synth.gen_embed(cfg, as_bits=bf))
+    head = dev(synth.gen_head(cfg, as_bits=bf))
+    W = dv.Weights(embed, head, layers)
+    s = synth.gen_sample(cfg, as_bits=bf)
+    n = cfg.n_seqs
+    dtype = dv.DAVET_BF16 if bf else dv.DAVET_F32
+    geoms, visual, view_bufs, sizes = [], [], [], []
+    tdt = torch.int16 if bf else torch.float32
+    for i in range(n):
+        g = dv.ViewGeom(s["n_crops"][i], cfg.grid, cfg.d, cfg.K, dtype)
+        sz = dv.davet_view_sizes(g)
+        geoms.append(g)
+        sizes.append(sz)
+        visual.append(dev(s["visual"][i]))
+        for lv in range(cfg.K - 1):
+            view_bufs.append(torch.empty((sz[lv], cfg.d), dtype=tdt,
+                                         device="cuda"))
+    prompt = torch.from_numpy(np.concatenate(s["prompts"])).cuda()
+    cu = [0]
+    for p in s["prompts"]:
+        cu.append(cu[-1] + len(p))
+    L = cfg.resp_len
+    mcfg = dv.ModelCfg(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn,
+                       cfg.vocab, cfg.mask_id, cfg.rms_eps, cfg.rope_theta,
+                       dtype)
+    max_tokens = sum(sz[-1] for sz in sizes) + cu[-1] + n * L
+    ws = torch.empty(dv.davet_workspace_bytes(mcfg, max_tokens, n, L),
+                     dtype=torch.uint8, device="cuda")
+    ids = torch.full((n * L,), cfg.mask_id, dtype=torch.int32, device="cuda")
+    msk = torch.ones((n * L,), dtype=torch.uint8, device="cuda")
+    pols, fixed = None, None
+    if cfg.schedule == "policy":
+        p = cfg.policy
+        pols = [dv.Policy(p["B"], p["rho"], p["alpha"],
+                          dv.davet_demand_prior(c), 1 if p["early"] else 0,
+                          cfg.K) for c in s["categories"]]
+    else:
+        fixed = s["schedule"]
+    torch.cuda.synchronize()
+    log("setup %.1f s (weights + inputs on device, workspace %.2f GB)"
+        % (time.time() - t0, ws.numel() / 1e9))
+    return dict(dv=dv, W=W, mcfg=mcfg, geoms=geoms, visual=visual,
+                view_bufs=view_bufs, prompt=prompt, cu=cu, L=L, ids=ids,
+                msk=msk, ws=ws, pols=pols, fixed=fixed, sizes=sizes,
+                sample=s)
+
+
+def run_loop(cfg, st):
+    st["ids"].fill_(cfg.mask_id)
+    st["msk"].fill_(1)
+    return st["dv"].davet_run_schedule(
+        st["mcfg"], st["W"], st["geoms"], st["visual"], st["view_bufs"],
+        st["prompt"], st["cu"], st["L"], cfg.steps, cfg.k, st["pols"],
+        st["fixed"], st["ids"], st["msk"], st["ws"])
+
+
+def work_per_loop(cfg, st, levels):
+    """Algorithmic work of one loop per kernel class: flops for matrix work,
+    bytes for the streaming kernels (views, head weight stream)."""
+    n, T, L, d, F, V = (cfg.n_seqs, cfg.steps, cfg.resp_len, cfg.d, cfg.ffn,
+                        cfg.vocab)
+    es = 2 if cfg.dtype == "bf16" else 4
+    w = {k: 0.0 for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down",
+                          "attention", "head_gemm_flops", "head_gemm_bytes",
+                          "views_bytes")}
+    for t in range(T):
+        ntot = 0
+        rows = 0
+        for s in range(n):
+            lv = levels[s * T + t]
+            N = st["sizes"][s][lv] + (st["cu"][s + 1] - st["cu"][s]) + L
+            ntot += N
+            w["attention"] += cfg.n_layers * 4.0 * N * N * d
+            rows += max(0, L - t * cfg.k)
+        w["gemm_qkv"] += cfg.n_layers * 2.0 * ntot * d * 3 * d
+        w["gemm_o"] += cfg.n_layers * 2.0 * ntot * d * d
+        w["gemm_gateup"] += cfg.n_layers * 2.0 * ntot * d * 2 * F
+        w["gemm_down"] += cfg.n_layers * 2.0 * ntot * F * d
+        w["head_gemm_flops"] += 2.0 * rows * d * V
+        w["head_gemm_bytes"] += float(V * d * es + rows * d * es)
+    for s in range(n):
+        sz = st["sizes"][s]
+        w["views_bytes"] += float((sz[-1] + sum(sz[:-1])) * d * es)
+    total_flops = sum(w[k] for k in ("gemm_qkv", "gemm_o", "gemm_gateup",
+                                     "gemm_down", "attention",
+                                     "head_gemm_flops"))
+    return w, total_flops
+
+
+def roofline(cfg, kern, work, loops):
+    """Roofline object of the kernel class that took the most time."""
+    mm = {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o",
+          "gemm_gateup": "gemm_gateup", "gemm_down": "gemm_down",
+          "attention": "attention", "gemm_f32": None, "attention_f32": None}
+    ranked = sorted(kern.items(), key=lambda kv: -kv[1][1])
+    for name, (cnt, ms) in ranked:
+        if cnt == 0:
+            continue
+        sec = ms / 1e3
+        if name in mm and mm[name]:
+            flops = work[mm[name]] * loops
+            peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
+            ach = flops / sec / 1e12
+            return dict(kernel=name, bound="mfma", achieved=round(ach, 2),
+                        peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
+                        traffic=None, launches=cnt,
+                        mean_launch_us=round(ms * 1e3 / cnt, 2))
+        if name == "head_gemm":
+            byts = work["head_gemm_bytes"] * loops
+            ach = byts / sec / 1e9
+            return dict(kernel=name, bound="hbm", achieved=round(ach, 1),
+                        peak=PEAK_HBM_GBS, unit="GB/s",
+                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=None,
+                        launches=cnt, mean_launch_us=round(ms * 1e3 / cnt, 2))
+    return None
+
+
+def cpu_baseline(cfg, st, n_layers_run):
+    """The oracle, as it stands, on this host: one step per level the
+    schedule uses (all positions masked, first sample), weighted by how
+    often the schedule uses each level."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle import model, views
+
+    levels = st["levels"]
+    T = cfg.steps
+    s0 = st["sample"]
+    visual = synth.gen_visual(cfg, s0["n_crops"][:1])[0]
+    lv_f, _ = views.build_views(visual, s0["n_crops"][0], cfg.grid, cfg.K,
+                                cfg.dtype)
+    host = dict(embed=synth.gen_embed(cfg), head=synth.gen_head(cfg),
+                layers=[synth.gen_layer_weights(cfg, i)
+                        for i in range(n_layers_run)])
+
+    class C:
+        pass
+    c = C()
+    for k in ("n_heads", "head_dim", "rms_eps", "rope_theta", "mask_id"):
+        setattr(c, k, getattr(cfg, k))
+    c.n_layers = n_layers_run
+    L = cfg.resp_len
+    used = sorted(set(levels[:T]))
+    per_level = {}
+    for lv in used:
+        t0 = time.perf_counter()
+        model.step_logits(c, lv_f[lv], s0["prompts"][0],
+                          np.full(L, cfg.mask_id), np.ones(L, np.uint8), host)
+        per_level[lv] = time.perf_counter() - t0
+    # extrapolate the layer stack when fewer layers ran than the model has
+    sec = 0.0
+    for t in range(T):
+        sec += per_level[levels[t]] * (cfg.n_layers / n_layers_run
+                                       if n_layers_run < cfg.n_layers else 1.0)
+    sec *= cfg.n_seqs
+    threads = 0
+    for info in threadpool_info():
+        if info.get("user_api") == "blas":
+            threads = max(threads, info.get("num_threads", 0))
+    sample = ("one oracle step per level %s of sample 0 (all positions "
+              "masked), float64 numpy, %d of %d layers run%s; weighted by the "
+              "schedule's %d steps%s" % (
+                  used, n_layers_run, cfg.n_layers,
+                  " (stack time extrapolated)"
+                  if n_layers_run < cfg.n_layers else "", T,
+                  " x %d samples" % cfg.n_seqs if cfg.n_seqs > 1 else ""))
+    return dict(value=round(T / sec, 4), unit="denoise steps/s",
+                cores=threads or len(os.sched_getaffinity(0)), kind="oracle",
+                sample=sample,
+                seconds_per_level={str(k): round(v, 3)
+                                   for k, v in per_level.items()})
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU "
+              "path (requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world),
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+
+    cfg = synth.get_config(args.config)
+    st = setup(cfg)
+    dv = st["dv"]
+    for _ in range(args.warmup):
+        run_loop(cfg, st)
+    torch.cuda.synchronize()
+
+    levels, _ = run_loop(cfg, st)          # schedule actually taken
+    torch.cuda.synchronize()
+    st["levels"] = levels
+    work, flops_loop = work_per_loop(cfg, st, levels)
+
+    if not args.no_kernel_timing:
+        launches = args.steps * cfg.steps * (12 * cfg.n_layers + 16) + 64
+        dv.prof_enable(launches)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_loop(cfg, st)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kern = {}
+    if not args.no_kernel_timing:
+        kern = dv.prof_read()
+        dv.prof_enable(0)
+    elapsed = t1 - t0
+    loops = args.steps
+    steps_per_s = loops * cfg.steps / elapsed
+    ms_loop = elapsed / loops * 1e3
+
+    rl = roofline(cfg, kern, work, loops) if kern else None
+    kernels = {k: dict(launches=c, total_ms=round(ms, 3),
+                       mean_us=round(ms * 1e3 / c, 2) if c else 0.0)
+               for k, (c, ms) in kern.items() if c}
+    cpu = None
+    if not args.no_cpu_baseline:
+        try:
+            cpu = cpu_baseline(cfg, st, max(1, min(args.cpu_layers,
+                                                   cfg.n_layers)))
+        except Exception as e:  # report, never hide, a failed baseline
+            cpu = dict(error=repr(e))
+    hist = {}
+    for lv in levels:
+        hist[str(lv)] = hist.get(str(lv), 0) + 1
+    out = {
+        "metric": "denoise steps/s + %bf16-MFMA-peak, 8B-shaped stack, "
+                  "729-3645 visual tokens",
+        "value": round(steps_per_s, 3),
+        "unit": "denoise steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_loop, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) visual "
+                "encodings, uniform prompt ids)",
+        "config": {
+            "workload": cfg.name,
+            "n_layers": cfg.n_layers, "d": cfg.d, "heads": cfg.n_heads,
+            "head_dim": cfg.head_dim, "ffn": cfg.ffn, "vocab": cfg.vocab,
+            "visual_tokens": [sz[-1] for sz in st["sizes"]],
+            "view_levels_tokens": st["sizes"][0],
+            "prompt": [st["cu"][i + 1] - st["cu"][i]
+                       for i in range(cfg.n_seqs)],
+            "response": cfg.resp_len, "denoise_steps_per_step": cfg.steps,
+            "commit_per_step": cfg.k, "n_seqs": cfg.n_seqs,
+            "schedule": cfg.schedule, "level_histogram": hist,
+            "parallelism": "none (one GPU)",
+        },
+        "ms_per_denoise_step": round(ms_loop / cfg.steps, 4),
+        "tflops_algorithmic": round(flops_loop * loops / elapsed / 1e12, 2),
+        "roofline": rl,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,18 +1,23 @@
 """Seeded generators for the synthetic workloads (no method arithmetic here).
 
-Seeds: ``1000 * cid + stream``.  Streams: 0 layer weights (``+16 * layer``),
-1 visual encoding, 2 prompt ids, 3 schedule, 4 batch shapes, 5 token
-embedding, 6 output head.  Weights, embedding and head are N(0, 0.02^2);
+Seeds: ``1000 * cid + stream``.  Streams: 0 layer weights (``+16 * layer``,
+keyed by tensor), 1 visual encoding (keyed by sample), 2 prompt ids,
+3 schedule, 4 batch shapes, 5 token embedding, 6 output head.  Normal draws
+are made in independently seeded chunks (numpy SeedSequence spawn keys) so
+they can be filled by several threads with the same result.  Weights, embedding and head are N(0, 0.02^2);
 visual encodings are N(0, 1); prompt ids are uniform over [0, V-1) so that
 the mask id V-1 never appears in a prompt.  The bf16 configurations round
 every drawn value to bfloat16 (RNE) before either side sees it.
 """
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 from .configs import Config
 
-_CHUNK = 1 << 24
+_CHUNK = 1 << 22
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -35,14 +40,31 @@ def _rng(cfg: Config, stream: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(1000 * cfg.cid + stream))
 
 
-def _normal(rng, n, std, dtype, as_bits):
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        n = max(1, min(16, len(os.sched_getaffinity(0))))
+        _POOL = ThreadPoolExecutor(n)
+    return _POOL
+
+
+def _normal(seed, key, n, std, dtype, as_bits):
     """n draws of std*N(0,1) in float32; bf16 bits when as_bits, else float32
-    (bf16-rounded when dtype == 'bf16')."""
+    (bf16-rounded when dtype == 'bf16').  Chunk c of 2^22 values comes from
+    PCG64(SeedSequence(seed, spawn_key=key + (c,))), so the values do not
+    depend on how many threads fill them."""
     out = np.empty(n, dtype=np.uint16 if as_bits else np.float32)
     s = np.float32(std)
-    for i in range(0, n, _CHUNK):
+
+    def fill(c):
+        i = c * _CHUNK
         m = min(_CHUNK, n - i)
-        z = rng.standard_normal(m, dtype=np.float32)
+        ss = np.random.SeedSequence(seed, spawn_key=tuple(key) + (c,))
+        z = np.random.Generator(np.random.PCG64(ss)).standard_normal(
+            m, dtype=np.float32)
         if s != 1.0:
             z *= s
         if as_bits:
@@ -51,6 +73,8 @@ def _normal(rng, n, std, dtype, as_bits):
             out[i:i + m] = round_to_bf16(z)
         else:
             out[i:i + m] = z
+
+    list(_pool().map(fill, range((n + _CHUNK - 1) // _CHUNK)))
     return out
 
 
@@ -61,26 +85,29 @@ def gen_layer_weights(cfg: Config, layer: int, as_bits: bool = False):
     wo [d, d], wg [F, d], wu [F, d], wd [d, F]; all row-major, out = x @ W^T.
     Norm gains are 1 and are not drawn.
     """
-    rng = np.random.Generator(np.random.PCG64(1000 * cfg.cid + 16 * layer))
+    seed = 1000 * cfg.cid + 16 * layer
     d, F = cfg.d, cfg.ffn
     shapes = dict(wqkv=(3 * d, d), wo=(d, d), wg=(F, d), wu=(F, d), wd=(d, F))
     out = {}
-    for name, shp in shapes.items():
-        out[name] = _normal(rng, shp[0] * shp[1], cfg.weight_std, cfg.dtype,
-                            as_bits and cfg.dtype == "bf16").reshape(shp)
+    for j, (name, shp) in enumerate(shapes.items()):
+        out[name] = _normal(seed, (j,), shp[0] * shp[1], cfg.weight_std,
+                            cfg.dtype, as_bits and cfg.dtype == "bf16"
+                            ).reshape(shp)
     return out
 
 
 def gen_embed(cfg: Config, as_bits: bool = False) -> np.ndarray:
     """Token embedding E [V, d]."""
-    return _normal(_rng(cfg, 5), cfg.vocab * cfg.d, cfg.weight_std, cfg.dtype,
-                   as_bits and cfg.dtype == "bf16").reshape(cfg.vocab, cfg.d)
+    return _normal(1000 * cfg.cid + 5, (), cfg.vocab * cfg.d, cfg.weight_std,
+                   cfg.dtype, as_bits and cfg.dtype == "bf16"
+                   ).reshape(cfg.vocab, cfg.d)
 
 
 def gen_head(cfg: Config, as_bits: bool = False) -> np.ndarray:
     """Untied output head W_out [V, d]."""
-    return _normal(_rng(cfg, 6), cfg.vocab * cfg.d, cfg.weight_std, cfg.dtype,
-                   as_bits and cfg.dtype == "bf16").reshape(cfg.vocab, cfg.d)
+    return _normal(1000 * cfg.cid + 6, (), cfg.vocab * cfg.d, cfg.weight_std,
+                   cfg.dtype, as_bits and cfg.dtype == "bf16"
+                   ).reshape(cfg.vocab, cfg.d)
 
 
 def gen_batch_shapes(cfg: Config):
@@ -104,14 +131,14 @@ def gen_batch_shapes(cfg: Config):
 
 
 def gen_visual(cfg: Config, n_crops_list, as_bits: bool = False):
-    """Visual encodings v_s [n_crops_s * G * G, d] ~ N(0,1), drawn in
-    sample order from stream 1."""
-    rng = _rng(cfg, 1)
+    """Visual encodings v_s [n_crops_s * G * G, d] ~ N(0,1) from stream 1,
+    sample s keyed by its index."""
     out = []
-    for c in n_crops_list:
+    for i, c in enumerate(n_crops_list):
         n = c * cfg.grid * cfg.grid
-        out.append(_normal(rng, n * cfg.d, 1.0, cfg.dtype,
-                           as_bits and cfg.dtype == "bf16").reshape(n, cfg.d))
+        out.append(_normal(1000 * cfg.cid + 1, (i,), n * cfg.d, 1.0,
+                           cfg.dtype, as_bits and cfg.dtype == "bf16"
+                           ).reshape(n, cfg.d))
     return out
 
 
