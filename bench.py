@@ -54,10 +54,13 @@ def parse():
                     help="skip the per-launch HIP events")
     ap.add_argument("--cpu-layers", type=int, default=1,
                     help="layers the CPU oracle runs (extrapolated beyond)")
+    ap.add_argument("--mode", choices=["f16", "bf16"], default="f16",
+                    help="16-bit operand format for a bf16 model (f16: its "
+                         "weights converted exactly; default)")
     return ap.parse_args()
 
 
-def setup(cfg):
+def setup(cfg, mode):
     import numpy as np
     import torch
 
@@ -65,12 +68,22 @@ def setup(cfg):
     import synth
 
     t0 = time.time()
+    bf = cfg.dtype == "bf16"
+    dtype = {"f16": dv.DAVET_F16, "bf16": dv.DAVET_BF16}[mode] if bf \
+        else dv.DAVET_F32
 
     def dev(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)
-                                if bits.dtype == np.uint16 else bits).cuda()
+        """Upload; a bf16 tensor in fp16 mode is converted on the device."""
+        if bits.dtype != np.uint16:
+            return torch.from_numpy(bits).cuda()
+        t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+        if dtype == dv.DAVET_F16:
+            out = torch.empty_like(t)
+            dv.davet_convert(t, dv.DAVET_BF16, out, dv.DAVET_F16)
+            torch.cuda.synchronize()
+            return out
+        return t
 
-    bf = cfg.dtype == "bf16"
     layers = []
     for li in range(cfg.n_layers):
         lw = synth.gen_layer_weights(cfg, li, as_bits=bf)
@@ -81,7 +94,6 @@ def setup(cfg):
     W = dv.Weights(embed, head, layers)
     s = synth.gen_sample(cfg, as_bits=bf)
     n = cfg.n_seqs
-    dtype = dv.DAVET_BF16 if bf else dv.DAVET_F32
     geoms, visual, view_bufs, sizes = [], [], [], []
     tdt = torch.int16 if bf else torch.float32
     for i in range(n):
@@ -263,7 +275,8 @@ def main():
     import synth
 
     cfg = synth.get_config(args.config)
-    st = setup(cfg)
+    mode = args.mode if cfg.dtype == "bf16" else "f32"
+    st = setup(cfg, mode)
     dv = st["dv"]
     for _ in range(args.warmup):
         run_loop(cfg, st)
@@ -318,11 +331,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": cfg.dtype,
+        "dtype": mode,
         "data": "synthetic (seeded N(0,0.02) weights, N(0,1) visual "
                 "encodings, uniform prompt ids)",
         "config": {
-            "workload": cfg.name,
+            "workload": cfg.name, "model_dtype": cfg.dtype,
+            "operands": {"f16": "fp16 x fp16 -> fp32 matrix cores, bf16 "
+                                "weights converted exactly",
+                         "bf16": "bf16 x bf16 -> fp32 matrix cores",
+                         "f32": "fp32 vector ALU"}[mode],
             "n_layers": cfg.n_layers, "d": cfg.d, "heads": cfg.n_heads,
             "head_dim": cfg.head_dim, "ffn": cfg.ffn, "vocab": cfg.vocab,
             "visual_tokens": [sz[-1] for sz in st["sizes"]],

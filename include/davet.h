@@ -26,8 +26,13 @@
  *     call returns a negative davet_status, enqueues nothing, and
  *     davet_last_error() describes the failure (thread-local string).
  *   - Element types: DAVET_F32 = IEEE float32, DAVET_BF16 = bfloat16 bit
- *     patterns (uint16).  Residual streams, softmax and norms run in float32
- *     in both modes; bf16 mode feeds bf16 operands to the matrix cores.
+ *     patterns, DAVET_F16 = IEEE binary16 bit patterns (both uint16).  The
+ *     16-bit modes feed 16-bit operands of that type to the matrix cores with
+ *     float32 accumulation; residual streams, softmax statistics and norms
+ *     run in float32 in every mode.  A bf16 model runs in either 16-bit
+ *     mode: its weights convert to fp16 exactly (davet_convert) whenever
+ *     |w| >= 2^-17, and fp16 operands carry 3 more mantissa bits through
+ *     the activations at the same matrix-core rate.
  */
 #ifndef DAVET_H
 #define DAVET_H
@@ -49,7 +54,7 @@ typedef enum davet_status {
   DAVET_EHIP = -5      /* a HIP runtime call failed                         */
 } davet_status;
 
-typedef enum davet_dtype { DAVET_F32 = 0, DAVET_BF16 = 1 } davet_dtype;
+typedef enum davet_dtype { DAVET_F32 = 0, DAVET_BF16 = 1, DAVET_F16 = 2 } davet_dtype;
 
 /* Limits of this build. */
 #define DAVET_MAX_SEQS 64        /* sequences per packed batch            */
@@ -67,8 +72,9 @@ typedef struct davet_view_geom {
   int32_t dtype;      /* davet_dtype of v and of the pooled levels */
 } davet_view_geom;
 
-/* Denoiser shape.  d = n_heads * head_dim, head_dim in {64, 128}; d and ffn
- * multiples of 256 (bf16) or 64 (f32); mask_id in [0, vocab). */
+/* Denoiser shape.  d = n_heads * head_dim, head_dim in {64, 128} (128 in the
+ * 16-bit modes, where d must be a multiple of 128 and ffn of 64); d <= 8192;
+ * mask_id in [0, vocab). */
 typedef struct davet_model_cfg {
   int32_t n_layers;
   int32_t d;
@@ -147,6 +153,13 @@ int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens /*host[K]*/);
 int davet_build_views(const davet_view_geom* g, const void* v,
                       void* const* levels, int32_t* const* idx_offsets,
                       int32_t* const* idx_members, hipStream_t stream);
+
+/* Element-type conversion of n values, rounding to nearest even (e.g. a bf16
+ * checkpoint into the fp16 operand mode: exact whenever |x| >= 2^-17 and
+ * |x| <= 65504).  src and dst are device buffers of n elements of their
+ * dtypes and must not overlap.  Errors: EINVAL (null, overlap), EDTYPE. */
+int davet_convert(const void* src, int32_t src_dtype, void* dst,
+                  int32_t dst_dtype, size_t n, hipStream_t stream);
 
 /* ------------------------------------------------------------- denoiser -- */
 

@@ -60,7 +60,7 @@ def pool_level(v: np.ndarray, n_crops: int, grid: int, K: int, level: int,
                out_dtype: str = "f32") -> np.ndarray:
     """Level ``level`` of the hierarchy: each token is the float64 sum of its
     members (taken in index-map order) divided by the member count, rounded
-    once to the output precision (fp32, or bf16 for bf16 encodings)."""
+    once to the output precision (fp32, bf16 or fp16, as the encoding)."""
     offs, mem = index_map(n_crops, grid, K, level)
     v64 = np.asarray(v, dtype=np.float64)
     n = len(offs) - 1
@@ -72,6 +72,10 @@ def pool_level(v: np.ndarray, n_crops: int, grid: int, K: int, level: int,
         out[t] = acc / float(offs[t + 1] - offs[t])
     if out_dtype == "bf16":
         return _round_f64_to_bf16(out)
+    if out_dtype == "f16":
+        # numpy converts float64 to binary16 directly (one rounding, ties to
+        # even, subnormals included)
+        return out.astype(np.float16).astype(np.float32)
     return out.astype(np.float32)
 
 

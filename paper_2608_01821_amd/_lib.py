@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libdavet.so")
 
 DAVET_F32 = 0
 DAVET_BF16 = 1
+DAVET_F16 = 2
 MAX_SEQS = 64
 
 
@@ -57,7 +58,7 @@ class Policy(C.Structure):
 
 if not os.path.exists(LIB_PATH):
     raise ImportError("libdavet.so is not built (%s); run "
-                      "`python -m paper_2608_01821_amd.build`" % LIB_PATH)
+                      "`python paper_2608_01821_amd/build.py`" % LIB_PATH)
 _L = C.CDLL(LIB_PATH)
 
 _vp = C.c_void_p
@@ -73,6 +74,7 @@ _SIGS = {
     "davet_view_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
     "davet_build_views": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
                                     _P_vp, _vp]),
+    "davet_convert": (C.c_int, [_vp, _i32, _vp, _i32, C.c_size_t, _vp]),
     "davet_workspace_bytes": (C.c_int, [C.POINTER(ModelCfg), _i32, _i32, _i32,
                                         C.POINTER(C.c_size_t)]),
     "davet_denoise_step": (C.c_int, [C.POINTER(ModelCfg), C.POINTER(WeightsT),
@@ -188,6 +190,12 @@ def davet_build_views(geom, v, levels, offsets=None, members=None,
     mem = _ptr_array(members) if members is not None else None
     _check(_L.davet_build_views(C.byref(geom), _ptr(v), lv, off, mem,
                                 _stream(stream)))
+
+
+def davet_convert(src, src_dtype, dst, dst_dtype, n=None, stream=None):
+    n = src.numel() if n is None else n
+    _check(_L.davet_convert(_ptr(src), int(src_dtype), _ptr(dst),
+                            int(dst_dtype), int(n), _stream(stream)))
 
 
 def davet_workspace_bytes(cfg, max_tokens, max_seqs, L):

@@ -3,7 +3,8 @@
 Device sources (*.hip) and the HIP-runtime host sources are compiled with
 hipcc for gfx950 only; the allocation policy is compiled with g++ and
 -ffp-contract=off so its double arithmetic is never contracted into fused
-multiply-adds.  Usage: ``python -m paper_2608_01821_amd.build``.
+multiply-adds.  Usage: ``python paper_2608_01821_amd/build.py`` (run by
+path: importing the package would load the old library first).
 """
 
 import concurrent.futures as cf
@@ -32,7 +33,7 @@ POLICY_FLAGS = [
     "-D__HIP_PLATFORM_AMD__",
 ]
 
-HIP_SOURCES = ["views.hip", "unmask.hip", "rowops.hip", "gemm_bf16.hip",
+HIP_SOURCES = ["views.hip", "unmask.hip", "rowops.hip", "gemm16.hip",
                "gemm_f32.hip", "attention.hip", "step.hip", "runtime.cpp",
                "schedule.cpp"]
 POLICY_SOURCES = ["policy.cpp"]

@@ -3,13 +3,14 @@
 // parallel through bidirectional attention).  Every query of a sequence sees
 // every key of the same sequence; sequences never mix.
 //
-// bf16 path, head_dim 128, CDNA4 matrix cores.  A workgroup of 4 wavefronts
-// owns 128 queries of one head; each wavefront owns 32 queries.  Keys stream
-// in tiles of 64 staged in LDS: K row-major, V transposed.  Per tile a
-// wavefront computes S^T = K Q^T (2 x 8 v_mfma_f32_32x32x16_bf16), so every
-// lane holds the scores of ONE query: the online-softmax rescale is a per-lane
-// scalar and the probabilities, rounded to bf16, are already laid out as the B
-// operand of O^T += V^T P^T (4 x 4 MFMAs) -- no LDS round trip for P.  Scores,
+// 16-bit path (bf16 or fp16 operands), head_dim 128, CDNA4 matrix cores.  A
+// workgroup of 4 wavefronts owns 128 queries of one head; each wavefront owns
+// 32 queries.  Keys stream in tiles of 64 staged in LDS: K row-major, V
+// transposed.  Per tile a wavefront computes S^T = K Q^T (2 x 8
+// v_mfma_f32_32x32x16 ops), so every lane holds the scores of ONE query: the
+// online-softmax rescale is a per-lane scalar and the probabilities, rounded
+// to 16 bits, are already laid out as the B operand of O^T += V^T P^T (4 x 4
+// MFMAs) -- no LDS round trip for P.  Scores,
 // running max and normaliser stay in fp32 (exp2 with log2(e) folded into the
 // 1/sqrt(D) scale).  Ragged tails: keys past the sequence end score -inf;
 // queries past it are computed on clamped rows and never stored.
@@ -39,9 +40,11 @@ __device__ __forceinline__ void locate_tile(const SeqPack& sp, int tile,
   qt = tile - acc;
 }
 
+template <typename Fmt>
 __global__ void __launch_bounds__(256, 1)
-attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
-                 SeqPack sp, int n_heads, float scale_log2) {
+attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
+              SeqPack sp, int n_heads, float scale_log2) {
+  using v8 = typename Fmt::v8;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * K_STRIDE];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * V_STRIDE];
   int s, qt;
@@ -58,12 +61,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   const int qc = min(q, N - 1);
 
   // Q^T fragments (B operand): 8 k-steps of 16 head dims
-  bf16x8 qf[HD / 16];
+  v8 qf[HD / 16];
   {
     const uint16_t* qp = qkv + (size_t)(row0 + qc) * ld + (size_t)h * HD + hh * 8;
 #pragma unroll
     for (int ks = 0; ks < HD / 16; ++ks)
-      qf[ks] = __builtin_bit_cast(bf16x8,
+      qf[ks] = __builtin_bit_cast(v8,
                                   *reinterpret_cast<const u32x4*>(qp + ks * 16));
   }
   f32x16 o[HD / 32];
@@ -112,10 +115,10 @@ attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < HD / 16; ++ks) {
-        const bf16x8 kf = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(
-                        &Ks[(mt * 32 + l32) * K_STRIDE + ks * 16 + hh * 8]));
-        sc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[mt], 0, 0, 0);
+        const v8 kf = __builtin_bit_cast(
+            v8, *reinterpret_cast<const u32x4*>(
+                    &Ks[(mt * 32 + l32) * K_STRIDE + ks * 16 + hh * 8]));
+        sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
       }
     }
     // ---- online softmax for this lane's query over its 32 keys + partner's 32
@@ -133,14 +136,14 @@ attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
     const float m_new = fmaxf(m_run, tmax);
     const float alpha = exp2f(m_run - m_new);
     float psum = 0.f;
-    bf16x8 pf[4];
+    uint16_t pb[4][8];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const float p = exp2f(sc[mt][e] - m_new);
         psum += p;
-        pf[mt * 2 + (e >> 3)][e & 7] = (__bf16)p;
+        pb[mt * 2 + (e >> 3)][e & 7] = Fmt::store(p);
       }
     psum += __shfl_xor(psum, 32, 64);
     l_run = l_run * alpha + psum;
@@ -161,8 +164,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
         const u32x2 v1 = *reinterpret_cast<const u32x2*>(vr + 8);
         u32x4 vv;
         vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8, vv), pf[ps], o[dt], 0, 0, 0);
+        u32x4 pw;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          pw[q] = (uint32_t)pb[ps][2 * q] | ((uint32_t)pb[ps][2 * q + 1] << 16);
+        o[dt] = Fmt::mfma32(__builtin_bit_cast(v8, vv),
+                            __builtin_bit_cast(v8, pw), o[dt]);
       }
     }
     __syncthreads();
@@ -177,10 +184,10 @@ attn_bf16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       for (int g = 0; g < 4; ++g) {
         const int dd = dt * 32 + g * 8 + hh * 4;
         u32x2 w;
-        w[0] = (uint32_t)f32_to_bf16(o[dt][g * 4 + 0] * inv) |
-               ((uint32_t)f32_to_bf16(o[dt][g * 4 + 1] * inv) << 16);
-        w[1] = (uint32_t)f32_to_bf16(o[dt][g * 4 + 2] * inv) |
-               ((uint32_t)f32_to_bf16(o[dt][g * 4 + 3] * inv) << 16);
+        w[0] = (uint32_t)Fmt::store(o[dt][g * 4 + 0] * inv) |
+               ((uint32_t)Fmt::store(o[dt][g * 4 + 1] * inv) << 16);
+        w[1] = (uint32_t)Fmt::store(o[dt][g * 4 + 2] * inv) |
+               ((uint32_t)Fmt::store(o[dt][g * 4 + 3] * inv) << 16);
         *reinterpret_cast<u32x2*>(op + dd) = w;
       }
   }
@@ -226,18 +233,23 @@ attn_f32_kernel(const float* __restrict__ qkv, float* __restrict__ out,
 
 }  // namespace
 
-int launch_attention_bf16(const uint16_t* qkv, uint16_t* o, const SeqPack& sp,
-                          int n_heads, int head_dim, hipStream_t s) {
+int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
+                       const SeqPack& sp, int n_heads, int head_dim,
+                       hipStream_t s) {
   if (head_dim != HD)
-    return set_error(DAVET_ESHAPE, "attention_bf16: head_dim must be 128");
+    return set_error(DAVET_ESHAPE, "attention16: head_dim must be 128");
   int tiles = 0;
   for (int i = 0; i < sp.n_seqs; ++i)
     tiles += (sp.row0[i + 1] - sp.row0[i] + QT - 1) / QT;
   if (tiles == 0) return DAVET_OK;
   ProfScope ps(KC_ATTN, s);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3(tiles, n_heads), dim3(256), 0, s,
-                     qkv, o, sp, n_heads, scale_log2);
+  if (dtype == DAVET_F16)
+    hipLaunchKernelGGL(attn16_kernel<F16>, dim3(tiles, n_heads), dim3(256), 0,
+                       s, qkv, o, sp, n_heads, scale_log2);
+  else
+    hipLaunchKernelGGL(attn16_kernel<BF16>, dim3(tiles, n_heads), dim3(256), 0,
+                       s, qkv, o, sp, n_heads, scale_log2);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }

@@ -9,6 +9,7 @@
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -64,6 +65,61 @@ __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
   return (uint16_t)(__float_as_uint(f) >> 16);
 }
 
+// float64 -> float32 with round-to-odd: truncate toward zero and set the last
+// mantissa bit when inexact.  A later round-to-nearest-even to a format with
+// at least 2 fewer mantissa bits then equals one correct rounding of x.
+__device__ __forceinline__ float f64_to_f32_odd(double x) {
+  float f = (float)x;
+  const double back = (double)f;
+  if (back == x || x != x) return f;
+  if (fabs(back) > fabs(x))                       // rounded away from zero
+    f = __uint_as_float(__float_as_uint(f) - 1u);
+  return __uint_as_float(__float_as_uint(f) | 1u);
+}
+__device__ __forceinline__ uint16_t f32_to_f16(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);   // RNE
+}
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+// float64 -> fp16 with a single rounding (nearest even), subnormals included.
+__device__ __forceinline__ uint16_t f64_to_f16(double x) {
+  return f32_to_f16(f64_to_f32_odd(x));
+}
+
+// 16-bit operand formats of the matrix-core path.  Both are stored as
+// uint16_t bit patterns; fp32 accumulation in both.
+struct BF16 {
+  using v8 = bf16x8;
+  static constexpr int dtype = DAVET_BF16;
+  __device__ static __forceinline__ float load(uint16_t b) { return bf16_to_f32(b); }
+  __device__ static __forceinline__ uint16_t store(float f) { return f32_to_bf16(f); }
+  __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_bf16(x); }
+  __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+struct F16 {
+  using v8 = f16x8;
+  static constexpr int dtype = DAVET_F16;
+  __device__ static __forceinline__ float load(uint16_t h) { return f16_to_f32(h); }
+  __device__ static __forceinline__ uint16_t store(float f) { return f32_to_f16(f); }
+  __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_f16(x); }
+  __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+// Storage formats for row kernels: element type in memory plus conversions.
+struct F32S {
+  using st = float;
+  static constexpr int dtype = DAVET_F32;
+  __device__ static __forceinline__ float load(float x) { return x; }
+  __device__ static __forceinline__ float store(float x) { return x; }
+};
+struct BF16S : BF16 { using st = uint16_t; };
+struct F16S : F16 { using st = uint16_t; };
+
 __device__ __forceinline__ float warp_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -75,7 +131,8 @@ __device__ __forceinline__ float warp_max(float v) {
   return v;
 }
 
-inline size_t dtype_size(int dt) { return dt == DAVET_BF16 ? 2 : 4; }
+inline size_t dtype_size(int dt) { return dt == DAVET_F32 ? 4 : 2; }
+inline bool is16(int dt) { return dt == DAVET_BF16 || dt == DAVET_F16; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---- kernel launchers (host, defined next to their kernels) ----------------
@@ -125,21 +182,24 @@ int launch_head_reduce_f32(const float* logits, const int32_t* list,
 
 // GEMMs: C[M,N] = A[M,K] * B[N,K]^T
 enum Epilogue { EPI_STORE = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
-int launch_gemm_bf16(int epi, const uint16_t* A, const uint16_t* B,
-                     const uint16_t* B2, void* C, int M, int N, int K,
-                     int ldc, int cls, hipStream_t s);
-int launch_head_bf16(const uint16_t* Hm, const uint16_t* W, const int32_t* list,
-                     int max_rows, int vocab, int d, int mask_id, float* pmax,
-                     float* psum, int32_t* parg, float* logits_out,
-                     hipStream_t s);
-int head_bf16_slabs(int vocab);
+int launch_gemm16(int dtype, int epi, const uint16_t* A, const uint16_t* B,
+                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
+                  int cls, hipStream_t s);
+int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
+                  const int32_t* list, int max_rows, int vocab, int d,
+                  int mask_id, float* pmax, float* psum, int32_t* parg,
+                  float* logits_out, hipStream_t s);
+int head16_slabs(int vocab);
 int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     float* C, int M, int N, int K, int ldc, int cls,
                     const int32_t* m_count, hipStream_t s);
 
 // Attention over the packed batch: qkv [total, 3d] -> o [total, d]
-int launch_attention_bf16(const uint16_t* qkv, uint16_t* o, const SeqPack& sp,
-                          int n_heads, int head_dim, hipStream_t s);
+int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
+                       const SeqPack& sp, int n_heads, int head_dim,
+                       hipStream_t s);
+int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
+                   size_t n, hipStream_t s);
 int launch_attention_f32(const float* qkv, float* o, const SeqPack& sp,
                          int n_heads, int head_dim, hipStream_t s);
 

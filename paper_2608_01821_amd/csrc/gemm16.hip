@@ -1,4 +1,4 @@
-// bf16 matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] * B[N,K]^T with both
+// 16-bit (bf16 or fp16) matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] * B[N,K]^T with both
 // operands K-contiguous (activations row-major, weights [out, in]).
 //
 // Tiling for CDNA4: a 256-thread workgroup (4 wavefronts, 2 x 2) owns a
@@ -12,12 +12,12 @@
 // into one XCD's L2 and reused by every M tile of that column.
 //
 // Epilogues (fused, no extra pass over C):
-//   EPI_STORE    C bf16 = acc
+//   EPI_STORE    C (16-bit) = acc
 //   EPI_ADD_F32  C f32 += acc           (residual stream update)
 //   EPI_SWIGLU   dual weight: the tile's first BN/2 columns come from B (gate),
 //                the last BN/2 from B2 (up) at the same output index; the wave
 //                layout puts gate and up of one column in the same lane, so
-//                C bf16 = silu(gate) * up is formed in registers.
+//                C (16-bit) = silu(gate) * up is formed in registers.
 //   head         vocabulary slab reduction: per row, (max, first argmax, sum of
 //                exp(l - max)) over the slab's columns with [MASK] excluded.
 
@@ -48,9 +48,9 @@ __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
   return (bid & 7) * per + (bid >> 3);
 }
 
-template <int BM, int BN, int EPI>
+template <typename Fmt, int BM, int BN, int EPI>
 __global__ void __launch_bounds__(256, 1)
-gemm_bf16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
+gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
                  const uint16_t* __restrict__ B2, void* __restrict__ C, int M,
                  int N, int K, int ldc, int n_mtiles, HeadArgs ha) {
   constexpr int TM = BM / 64;            // 32-row sub-tiles per wave
@@ -139,27 +139,26 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     if (kt + 1 < nk) gload((kt + 1) * BK);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[TM], bfr[TN];
+      typename Fmt::v8 af[TM], bfr[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wm * (BM / 2) + i * 32 + lr;
         af[i] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(
+            typename Fmt::v8, *reinterpret_cast<const u32x4*>(
                         &As[cur][row * LDS_STRIDE + kk * 16 + lk]));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = j * 64 + wn * 32 + lr;
         bfr[j] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(
+            typename Fmt::v8, *reinterpret_cast<const u32x4*>(
                         &Bs[cur][row * LDS_STRIDE + kk * 16 + lk]));
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j],
-                                                              acc[i][j], 0, 0, 0);
+          acc[i][j] = Fmt::mfma32(af[i], bfr[j], acc[i][j]);
     }
     if (kt + 1 < nk) lstore(cur ^ 1);
     __syncthreads();
@@ -182,7 +181,7 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
           if (row < M) {
             if constexpr (EPI == EPI_STORE)
               reinterpret_cast<uint16_t*>(C)[(size_t)row * ldc + col] =
-                  f32_to_bf16(acc[i][j][e]);
+                  Fmt::store(acc[i][j][e]);
             else
               reinterpret_cast<float*>(C)[(size_t)row * ldc + col] +=
                   acc[i][j][e];
@@ -204,7 +203,7 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
             const float u = acc[i][j + TN / 2][e];
             const float h = g / (1.0f + __expf(-g)) * u;
             reinterpret_cast<uint16_t*>(C)[(size_t)row * ldc + col] =
-                f32_to_bf16(h);
+                Fmt::store(h);
           }
         }
       }
@@ -273,51 +272,68 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   }
 }
 
-template <int BM, int BN, int EPI>
+template <typename Fmt, int BM, int BN, int EPI>
 int launch(const uint16_t* A, const uint16_t* B, const uint16_t* B2, void* C,
            int M, int N, int K, int ldc, int n_ntiles, const HeadArgs& ha,
            hipStream_t s) {
   const int mt = (M + BM - 1) / BM;
   const int nwg = mt * n_ntiles;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI>), dim3(nwg), dim3(256), 0,
-                     s, A, B, B2, C, M, N, K, ldc, mt, ha);
+  hipLaunchKernelGGL((gemm16_kernel<Fmt, BM, BN, EPI>), dim3(nwg), dim3(256),
+                     0, s, A, B, B2, C, M, N, K, ldc, mt, ha);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
 
-}  // namespace
-
-int launch_gemm_bf16(int epi, const uint16_t* A, const uint16_t* B,
-                     const uint16_t* B2, void* C, int M, int N, int K, int ldc,
-                     int cls, hipStream_t s) {
-  if (M <= 0) return DAVET_OK;
-  if (N % 128 || K % BK)
-    return set_error(DAVET_ESHAPE, "gemm_bf16: N % 128 or K % 64 != 0");
-  ProfScope ps(cls, s);
+template <typename Fmt>
+int gemm_dispatch(int epi, const uint16_t* A, const uint16_t* B,
+                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
+                  hipStream_t s) {
   HeadArgs ha{};
   switch (epi) {
     case EPI_STORE:
-      return launch<128, 128, EPI_STORE>(A, B, B2, C, M, N, K, ldc, N / 128, ha, s);
+      return launch<Fmt, 128, 128, EPI_STORE>(A, B, B2, C, M, N, K, ldc,
+                                              N / 128, ha, s);
     case EPI_ADD_F32:
-      return launch<128, 128, EPI_ADD_F32>(A, B, B2, C, M, N, K, ldc, N / 128, ha, s);
+      return launch<Fmt, 128, 128, EPI_ADD_F32>(A, B, B2, C, M, N, K, ldc,
+                                                N / 128, ha, s);
     case EPI_SWIGLU:   // N = 2 * ffn output columns of gate|up
-      return launch<128, 128, EPI_SWIGLU>(A, B, B2, C, M, N, K, ldc, N / 128, ha, s);
+      return launch<Fmt, 128, 128, EPI_SWIGLU>(A, B, B2, C, M, N, K, ldc,
+                                               N / 128, ha, s);
   }
-  return set_error(DAVET_EINVAL, "gemm_bf16: unknown epilogue");
+  return set_error(DAVET_EINVAL, "gemm16: unknown epilogue");
 }
 
-int head_bf16_slabs(int vocab) { return (vocab + 127) / 128; }
+}  // namespace
 
-int launch_head_bf16(const uint16_t* Hm, const uint16_t* W, const int32_t* list,
-                     int max_rows, int vocab, int d, int mask_id, float* pmax,
-                     float* psum, int32_t* parg, float* logits_out,
-                     hipStream_t s) {
-  if (d % BK) return set_error(DAVET_ESHAPE, "head_bf16: d % 64 != 0");
+int launch_gemm16(int dtype, int epi, const uint16_t* A, const uint16_t* B,
+                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
+                  int cls, hipStream_t s) {
+  if (M <= 0) return DAVET_OK;
+  if (N % 128 || K % BK)
+    return set_error(DAVET_ESHAPE, "gemm16: N % 128 or K % 64 != 0");
+  ProfScope ps(cls, s);
+  return dtype == DAVET_F16
+             ? gemm_dispatch<F16>(epi, A, B, B2, C, M, N, K, ldc, s)
+             : gemm_dispatch<BF16>(epi, A, B, B2, C, M, N, K, ldc, s);
+}
+
+int head16_slabs(int vocab) { return (vocab + 127) / 128; }
+
+int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
+                  const int32_t* list, int max_rows, int vocab, int d,
+                  int mask_id, float* pmax, float* psum, int32_t* parg,
+                  float* logits_out, hipStream_t s) {
+  if (d % BK) return set_error(DAVET_ESHAPE, "head16: d % 64 != 0");
   ProfScope ps(KC_HEAD, s);
-  HeadArgs ha{list, vocab, mask_id, head_bf16_slabs(vocab), pmax, psum, parg,
+  HeadArgs ha{list, vocab, mask_id, head16_slabs(vocab), pmax, psum, parg,
               logits_out};
-  return launch<128, 128, EPI_HEAD>(Hm, W, nullptr, nullptr, max_rows, vocab,
-                                    d, 0, ha.n_slabs, ha, s);
+  return dtype == DAVET_F16
+             ? launch<F16, 128, 128, EPI_HEAD>(Hm, W, nullptr, nullptr,
+                                               max_rows, vocab, d, 0,
+                                               ha.n_slabs, ha, s)
+             : launch<BF16, 128, 128, EPI_HEAD>(Hm, W, nullptr, nullptr,
+                                                max_rows, vocab, d, 0,
+                                                ha.n_slabs, ha, s);
 }
 
 }  // namespace davet

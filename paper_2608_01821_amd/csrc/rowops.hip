@@ -4,6 +4,8 @@
 // merge.  One workgroup (4 wavefronts) per row; reductions are wavefront
 // butterflies followed by a 4-entry LDS combine.
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace davet {
@@ -29,27 +31,10 @@ __device__ __forceinline__ int find_seq(const SeqPack& sp, int row) {
   return s;
 }
 
-template <typename T>
-__device__ __forceinline__ float load_elem(const T* p, int i);
-template <>
-__device__ __forceinline__ float load_elem<float>(const float* p, int i) { return p[i]; }
-template <>
-__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int i) {
-  return bf16_to_f32(p[i]);
-}
-template <typename T>
-__device__ __forceinline__ void store_elem(T* p, int i, float v);
-template <>
-__device__ __forceinline__ void store_elem<float>(float* p, int i, float v) { p[i] = v; }
-template <>
-__device__ __forceinline__ void store_elem<uint16_t>(uint16_t* p, int i, float v) {
-  p[i] = f32_to_bf16(v);
-}
-
 constexpr int kMaxPer = 32;   // d <= 8192 elements per row
 
 // X[row] = [view | E[prompt] | E[resp or mask]] row; A[row] = RMSNorm(X[row]).
-template <typename T>
+template <typename Fmt, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
                      const int32_t* __restrict__ prompt_ids,
@@ -80,7 +65,7 @@ assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
 #pragma unroll
   for (int n = 0; n < kMaxPer; ++n) {
     const int e = threadIdx.x + n * kThreads;
-    x[n] = e < d ? load_elem(src, e) : 0.f;
+    x[n] = e < d ? Fmt::load(src[e]) : 0.f;
     ss += x[n] * x[n];
   }
   const float tot = block_sum(ss, red);
@@ -91,11 +76,11 @@ assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
     if (e >= d) break;
     X[(size_t)row * d + e] = x[n];
     const float g = gain ? gain[e] : 1.0f;
-    store_elem(A + (size_t)row * d, e, x[n] * rstd * g);
+    A[(size_t)row * d + e] = Fmt::store(x[n] * rstd * g);
   }
 }
 
-template <typename T>
+template <typename Fmt, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 rmsnorm_kernel(const float* __restrict__ X, int d,
                const float* __restrict__ gain, float eps, T* __restrict__ A) {
@@ -117,7 +102,7 @@ rmsnorm_kernel(const float* __restrict__ X, int d,
     const int e = threadIdx.x + n * kThreads;
     if (e >= d) break;
     const float g = gain ? gain[e] : 1.0f;
-    store_elem(A + (size_t)row * d, e, v[n] * rstd * g);
+    A[(size_t)row * d + e] = Fmt::store(v[n] * rstd * g);
   }
 }
 
@@ -135,7 +120,7 @@ __global__ void rope_table_kernel(int max_pos, int head_dim, double theta,
 
 // In-place rotary embedding of the query and key parts of qkv [rows, 3d]:
 // dim i pairs with dim i + D/2 inside each head (rotate-half form).
-template <typename T>
+template <typename Fmt, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
             const float2* __restrict__ cs) {
@@ -152,9 +137,9 @@ rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
     const int i = p % half;
     T* x = base + which * d + h * head_dim;
     const float2 c = cs[(size_t)pos * half + i];
-    const float a = load_elem(x, i), b = load_elem(x, i + half);
-    store_elem(x, i, a * c.x - b * c.y);
-    store_elem(x, i + half, b * c.x + a * c.y);
+    const float a = Fmt::load(x[i]), b = Fmt::load(x[i + half]);
+    x[i] = Fmt::store(a * c.x - b * c.y);
+    x[i + half] = Fmt::store(b * c.x + a * c.y);
   }
 }
 
@@ -195,7 +180,7 @@ head_prep_kernel(int total, const uint8_t* __restrict__ masked,
 }
 
 // Hm[j] = RMSNorm_final(X[packed row of masked position list[1+j]]).
-template <typename T>
+template <typename Fmt, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 final_norm_gather_kernel(const float* __restrict__ X, SeqPack sp,
                          const int32_t* __restrict__ list, int d,
@@ -223,7 +208,7 @@ final_norm_gather_kernel(const float* __restrict__ X, SeqPack sp,
     const int e = threadIdx.x + n * kThreads;
     if (e >= d) break;
     const float gg = gain ? gain[e] : 1.0f;
-    store_elem(Hm + (size_t)j * d, e, v[n] * rstd * gg);
+    Hm[(size_t)j * d + e] = Fmt::store(v[n] * rstd * gg);
   }
 }
 
@@ -316,7 +301,44 @@ head_reduce_f32_kernel(const float* __restrict__ logits,
   }
 }
 
+// Element-type conversion through float32 (exact for the 16-bit sources),
+// rounding to nearest even into the destination format.
+template <typename Src, typename Dst>
+__global__ void __launch_bounds__(256)
+convert_kernel(const typename Src::st* __restrict__ src,
+               typename Dst::st* __restrict__ dst, size_t n) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += stride)
+    dst[i] = Dst::store(Src::load(src[i]));
+}
+
+template <typename Src>
+int convert_from(const void* src, void* dst, int dst_dtype, size_t n,
+                 hipStream_t s) {
+  const size_t blocks = std::min<size_t>((n + 255) / 256, 65536);
+#define CV(D)                                                           \
+  hipLaunchKernelGGL((convert_kernel<Src, D>), dim3(blocks), dim3(256), 0, s, \
+                     (const typename Src::st*)src, (D::st*)dst, n)
+  if (dst_dtype == DAVET_F16) CV(F16S);
+  else if (dst_dtype == DAVET_BF16) CV(BF16S);
+  else CV(F32S);
+#undef CV
+  return DAVET_OK;
+}
+
 }  // namespace
+
+int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
+                   size_t n, hipStream_t s) {
+  if (n == 0) return DAVET_OK;
+  ProfScope ps(KC_MISC, s);
+  if (src_dtype == DAVET_BF16) convert_from<BF16S>(src, dst, dst_dtype, n, s);
+  else if (src_dtype == DAVET_F16) convert_from<F16S>(src, dst, dst_dtype, n, s);
+  else convert_from<F32S>(src, dst, dst_dtype, n, s);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
 
 int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const void* embed, const int32_t* prompt_ids,
@@ -324,16 +346,14 @@ int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          int mask_id, int vocab, int d, const float* gain,
                          float eps, float* X, void* A, hipStream_t s) {
   ProfScope ps(KC_ASSEMBLE, s);
-  if (dtype == DAVET_BF16)
-    hipLaunchKernelGGL(assemble_norm_kernel<uint16_t>, dim3(sp.total),
-                       dim3(kThreads), 0, s, sp, vp,
-                       (const uint16_t*)embed, prompt_ids, resp_ids, masked,
-                       mask_id, vocab, d, gain, eps, X, (uint16_t*)A);
-  else
-    hipLaunchKernelGGL(assemble_norm_kernel<float>, dim3(sp.total),
-                       dim3(kThreads), 0, s, sp, vp, (const float*)embed,
-                       prompt_ids, resp_ids, masked, mask_id, vocab, d, gain,
-                       eps, X, (float*)A);
+#define ASM(F)                                                               \
+  hipLaunchKernelGGL(assemble_norm_kernel<F>, dim3(sp.total), dim3(kThreads),  \
+                     0, s, sp, vp, (const F::st*)embed, prompt_ids, resp_ids, \
+                     masked, mask_id, vocab, d, gain, eps, X, (F::st*)A)
+  if (dtype == DAVET_BF16) ASM(BF16S);
+  else if (dtype == DAVET_F16) ASM(F16S);
+  else ASM(F32S);
+#undef ASM
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -341,12 +361,13 @@ int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
 int launch_rmsnorm(const float* X, int rows, int d, const float* gain,
                    float eps, int dtype, void* A, hipStream_t s) {
   ProfScope ps(KC_RMSNORM, s);
-  if (dtype == DAVET_BF16)
-    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(rows), dim3(kThreads), 0,
-                       s, X, d, gain, eps, (uint16_t*)A);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(kThreads), 0, s,
-                       X, d, gain, eps, (float*)A);
+#define RMS(F)                                                             \
+  hipLaunchKernelGGL(rmsnorm_kernel<F>, dim3(rows), dim3(kThreads), 0, s, X, \
+                     d, gain, eps, (F::st*)A)
+  if (dtype == DAVET_BF16) RMS(BF16S);
+  else if (dtype == DAVET_F16) RMS(F16S);
+  else RMS(F32S);
+#undef RMS
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -364,13 +385,13 @@ int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
 int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
                 const SeqPack& sp, const float* cs, hipStream_t s) {
   ProfScope ps(KC_ROPE, s);
-  if (dtype == DAVET_BF16)
-    hipLaunchKernelGGL(rope_kernel<uint16_t>, dim3(rows), dim3(kThreads), 0, s,
-                       (uint16_t*)qkv, sp, n_heads, head_dim,
-                       (const float2*)cs);
-  else
-    hipLaunchKernelGGL(rope_kernel<float>, dim3(rows), dim3(kThreads), 0, s,
-                       (float*)qkv, sp, n_heads, head_dim, (const float2*)cs);
+#define ROPE(F)                                                             \
+  hipLaunchKernelGGL(rope_kernel<F>, dim3(rows), dim3(kThreads), 0, s,        \
+                     (F::st*)qkv, sp, n_heads, head_dim, (const float2*)cs)
+  if (dtype == DAVET_BF16) ROPE(BF16S);
+  else if (dtype == DAVET_F16) ROPE(F16S);
+  else ROPE(F32S);
+#undef ROPE
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -389,14 +410,14 @@ int launch_final_norm_gather(const float* X, const SeqPack& sp,
                              const float* gain, float eps, int dtype, void* Hm,
                              hipStream_t s) {
   ProfScope ps(KC_HEAD_PREP, s);
-  if (dtype == DAVET_BF16)
-    hipLaunchKernelGGL(final_norm_gather_kernel<uint16_t>, dim3(max_rows),
-                       dim3(kThreads), 0, s, X, sp, list, d, gain, eps,
-                       (uint16_t*)Hm);
-  else
-    hipLaunchKernelGGL(final_norm_gather_kernel<float>, dim3(max_rows),
-                       dim3(kThreads), 0, s, X, sp, list, d, gain, eps,
-                       (float*)Hm);
+#define FNG(F)                                                              \
+  hipLaunchKernelGGL(final_norm_gather_kernel<F>, dim3(max_rows),            \
+                     dim3(kThreads), 0, s, X, sp, list, d, gain, eps,         \
+                     (F::st*)Hm)
+  if (dtype == DAVET_BF16) FNG(BF16S);
+  else if (dtype == DAVET_F16) FNG(F16S);
+  else FNG(F32S);
+#undef FNG
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -424,3 +445,21 @@ int launch_head_reduce_f32(const float* logits, const int32_t* list,
 }
 
 }  // namespace davet
+
+extern "C" int davet_convert(const void* src, int32_t src_dtype, void* dst,
+                             int32_t dst_dtype, size_t n, hipStream_t stream) {
+  using namespace davet;
+  DAVET_CHECK_ARG(n == 0 || (src && dst), DAVET_EINVAL,
+                  "davet_convert: null pointer");
+  auto ok = [](int t) {
+    return t == DAVET_F32 || t == DAVET_BF16 || t == DAVET_F16;
+  };
+  DAVET_CHECK_ARG(ok(src_dtype) && ok(dst_dtype), DAVET_EDTYPE,
+                  "davet_convert: unknown dtype");
+  const char* s0 = static_cast<const char*>(src);
+  const char* d0 = static_cast<const char*>(dst);
+  const size_t sb = n * dtype_size(src_dtype), db = n * dtype_size(dst_dtype);
+  DAVET_CHECK_ARG(s0 + sb <= d0 || d0 + db <= s0, DAVET_EINVAL,
+                  "davet_convert: src and dst overlap");
+  return launch_convert(src, src_dtype, dst, dst_dtype, n, stream);
+}

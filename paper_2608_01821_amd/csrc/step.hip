@@ -32,7 +32,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
                           int64_t seqs, int64_t L) {
   const size_t es = dtype_size(c.dtype);
   const int64_t rows = seqs * L;
-  const int64_t slabs = head_bf16_slabs(c.vocab);
+  const int64_t slabs = head16_slabs(c.vocab);
   Layout o{};
   size_t p = 0;
   auto take = [&](size_t bytes) {
@@ -50,7 +50,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   o.rope = take((size_t)tokens * (c.head_dim / 2) * 8);
   o.list = take((size_t)(rows + 1) * 4);
   o.Hm = take((size_t)rows * c.d * es);
-  if (c.dtype == DAVET_BF16) {
+  if (is16(c.dtype)) {
     o.pmax = take((size_t)rows * slabs * 4);
     o.psum = take((size_t)rows * slabs * 4);
     o.parg = take((size_t)rows * slabs * 4);
@@ -64,8 +64,8 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
 
 static int check_cfg(const davet_model_cfg* c) {
   DAVET_CHECK_ARG(c, DAVET_EINVAL, "model cfg is null");
-  DAVET_CHECK_ARG(c->dtype == DAVET_F32 || c->dtype == DAVET_BF16, DAVET_EDTYPE,
-                  "cfg.dtype must be DAVET_F32 or DAVET_BF16");
+  DAVET_CHECK_ARG(c->dtype == DAVET_F32 || is16(c->dtype), DAVET_EDTYPE,
+                  "cfg.dtype must be DAVET_F32, DAVET_BF16 or DAVET_F16");
   DAVET_CHECK_ARG(c->n_layers >= 0 && c->n_heads >= 1, DAVET_ESHAPE,
                   "cfg: n_layers >= 0 and n_heads >= 1 required");
   DAVET_CHECK_ARG(c->head_dim == 64 || c->head_dim == 128, DAVET_ESHAPE,
@@ -78,11 +78,11 @@ static int check_cfg(const davet_model_cfg* c) {
                   DAVET_ESHAPE, "cfg: vocab >= 2 and 0 <= mask_id < vocab");
   DAVET_CHECK_ARG(c->rms_eps >= 0.f && c->rope_theta > 0.f, DAVET_EINVAL,
                   "cfg: rms_eps >= 0 and rope_theta > 0 required");
-  if (c->dtype == DAVET_BF16) {
+  if (is16(c->dtype)) {
     DAVET_CHECK_ARG(c->head_dim == 128, DAVET_ESHAPE,
-                    "bf16 path: head_dim must be 128");
+                    "16-bit path: head_dim must be 128");
     DAVET_CHECK_ARG(c->d % 128 == 0 && c->ffn % 64 == 0 && (3 * c->d) % 128 == 0,
-                    DAVET_ESHAPE, "bf16 path: d % 128 == 0 and ffn % 64 == 0");
+                    DAVET_ESHAPE, "16-bit path: d % 128 == 0 and ffn % 64 == 0");
   }
   return DAVET_OK;
 }
@@ -197,7 +197,8 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
   void* Hm = ws + lay.Hm;
   const int rows = n_seqs * L;
-  const bool bf = c.dtype == DAVET_BF16;
+  const bool bf = is16(c.dtype);
+  const int dt = c.dtype;
   const int d = c.d, F = c.ffn;
   hipStream_t s = stream;
 
@@ -213,20 +214,20 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
     if (l > 0) RUN(launch_rmsnorm(X, sp.total, d, lw.attn_norm, c.rms_eps,
                                   c.dtype, A, s));
     if (bf) {
-      RUN(launch_gemm_bf16(EPI_STORE, (const uint16_t*)A,
+      RUN(launch_gemm16(dt, EPI_STORE, (const uint16_t*)A,
                            (const uint16_t*)lw.wqkv, nullptr, QKV, sp.total,
                            3 * d, d, 3 * d, KC_GEMM_QKV, s));
       RUN(launch_rope(QKV, sp.total, c.n_heads, c.head_dim, c.dtype, sp, rope, s));
-      RUN(launch_attention_bf16((const uint16_t*)QKV, (uint16_t*)O, sp,
-                                c.n_heads, c.head_dim, s));
-      RUN(launch_gemm_bf16(EPI_ADD_F32, (const uint16_t*)O,
+      RUN(launch_attention16(dt, (const uint16_t*)QKV, (uint16_t*)O, sp,
+                             c.n_heads, c.head_dim, s));
+      RUN(launch_gemm16(dt, EPI_ADD_F32, (const uint16_t*)O,
                            (const uint16_t*)lw.wo, nullptr, X, sp.total, d, d,
                            d, KC_GEMM_O, s));
       RUN(launch_rmsnorm(X, sp.total, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
-      RUN(launch_gemm_bf16(EPI_SWIGLU, (const uint16_t*)A,
+      RUN(launch_gemm16(dt, EPI_SWIGLU, (const uint16_t*)A,
                            (const uint16_t*)lw.wg, (const uint16_t*)lw.wu, H,
                            sp.total, 2 * F, d, F, KC_GEMM_GATEUP, s));
-      RUN(launch_gemm_bf16(EPI_ADD_F32, (const uint16_t*)H,
+      RUN(launch_gemm16(dt, EPI_ADD_F32, (const uint16_t*)H,
                            (const uint16_t*)lw.wd, nullptr, X, sp.total, d, F,
                            d, KC_GEMM_DOWN, s));
     } else {
@@ -249,13 +250,13 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
                                c.dtype, Hm, s));
   if (bf) {
-    const int slabs = head_bf16_slabs(c.vocab);
+    const int slabs = head16_slabs(c.vocab);
     float* pmax = reinterpret_cast<float*>(ws + lay.pmax);
     float* psum = reinterpret_cast<float*>(ws + lay.psum);
     int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);
-    RUN(launch_head_bf16((const uint16_t*)Hm, (const uint16_t*)w->head, list,
-                         rows, c.vocab, d, c.mask_id, pmax, psum, parg,
-                         logits_out, s));
+    RUN(launch_head16(dt, (const uint16_t*)Hm, (const uint16_t*)w->head, list,
+                      rows, c.vocab, d, c.mask_id, pmax, psum, parg,
+                      logits_out, s));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {

@@ -13,10 +13,12 @@ namespace {
 
 struct LevelOut { void* p[DAVET_MAX_LEVELS]; };
 
-template <int K, int VEC, typename T>
+
+template <int K, int VEC, typename Fmt>
 __global__ void __launch_bounds__(256)
-pool_views_kernel(const T* __restrict__ v, LevelOut out, int n_crops, int G,
-                  int d) {
+pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
+                  int n_crops, int G, int d) {
+  using T = typename Fmt::st;
   constexpr int F = 1 << (K - 1);                 // coarsest window side
   const int Wc = (G + F - 1) / F;
   const int win = blockIdx.x;                     // coarsest window id
@@ -49,13 +51,13 @@ pool_views_kernel(const T* __restrict__ v, LevelOut out, int n_crops, int G,
           u32x4 w = *reinterpret_cast<const u32x4*>(src);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            x[2 * q] = __uint_as_float(w[q] << 16);
-            x[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+            x[2 * q] = Fmt::load((uint16_t)(w[q] & 0xffffu));
+            x[2 * q + 1] = Fmt::load((uint16_t)(w[q] >> 16));
           }
         } else {
           uint32_t w = *reinterpret_cast<const uint32_t*>(src);
-          x[0] = __uint_as_float(w << 16);
-          x[1] = __uint_as_float(w & 0xffff0000u);
+          x[0] = Fmt::load((uint16_t)(w & 0xffffu));
+          x[1] = Fmt::load((uint16_t)(w >> 16));
         }
       } else {
 #pragma unroll
@@ -99,7 +101,7 @@ pool_views_kernel(const T* __restrict__ v, LevelOut out, int n_crops, int G,
           uint16_t* dst = reinterpret_cast<uint16_t*>(out.p[l]) + tok * d + e0;
           uint16_t h[VEC];
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) h[e] = f64_to_bf16(ac[e] / cnt);
+          for (int e = 0; e < VEC; ++e) h[e] = Fmt::from_f64(ac[e] / cnt);
           if constexpr (VEC == 8) {
             u32x4 w;
 #pragma unroll
@@ -153,14 +155,25 @@ view_maps_kernel(MapOut mo, int n_crops, int G, int K) {
   }
 }
 
-template <int K, int VEC, typename T>
+template <int K, int VEC, typename Fmt>
 void launch_pool(const davet_view_geom& g, const void* v, const LevelOut& lo,
                  hipStream_t s) {
   constexpr int F = 1 << (K - 1);
   const int Wc = (g.grid + F - 1) / F;
   dim3 grid(g.n_crops * Wc * Wc, (g.d / VEC + 255) / 256);
-  hipLaunchKernelGGL((pool_views_kernel<K, VEC, T>), grid, dim3(256), 0, s,
-                     reinterpret_cast<const T*>(v), lo, g.n_crops, g.grid, g.d);
+  hipLaunchKernelGGL((pool_views_kernel<K, VEC, Fmt>), grid, dim3(256), 0, s,
+                     reinterpret_cast<const typename Fmt::st*>(v), lo,
+                     g.n_crops, g.grid, g.d);
+}
+
+template <typename Fmt>
+void launch_pool_k(const davet_view_geom& g, const void* v, const LevelOut& lo,
+                   hipStream_t s) {
+  switch (g.K) {
+    case 2: launch_pool<2, 8, Fmt>(g, v, lo, s); break;
+    case 3: launch_pool<3, 8, Fmt>(g, v, lo, s); break;
+    default: launch_pool<4, 2, Fmt>(g, v, lo, s); break;
+  }
 }
 
 }  // namespace
@@ -171,15 +184,9 @@ int launch_views(const davet_view_geom& g, const void* v, void* const* levels,
   LevelOut lo{};
   for (int l = 0; l < g.K - 1; ++l) lo.p[l] = levels[l];
   ProfScope ps(KC_VIEWS, s);
-  const bool bf = g.dtype == DAVET_BF16;
-  switch (g.K) {
-    case 2: bf ? launch_pool<2, 8, uint16_t>(g, v, lo, s)
-               : launch_pool<2, 8, float>(g, v, lo, s); break;
-    case 3: bf ? launch_pool<3, 8, uint16_t>(g, v, lo, s)
-               : launch_pool<3, 8, float>(g, v, lo, s); break;
-    default: bf ? launch_pool<4, 2, uint16_t>(g, v, lo, s)
-                : launch_pool<4, 2, float>(g, v, lo, s); break;
-  }
+  if (g.dtype == DAVET_BF16) launch_pool_k<BF16S>(g, v, lo, s);
+  else if (g.dtype == DAVET_F16) launch_pool_k<F16S>(g, v, lo, s);
+  else launch_pool_k<F32S>(g, v, lo, s);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -232,8 +239,9 @@ extern "C" int davet_build_views(const davet_view_geom* g, const void* v,
                   "davet_build_views: grid and n_crops must be >= 1");
   DAVET_CHECK_ARG(g->d >= 8 && g->d % 8 == 0, DAVET_ESHAPE,
                   "davet_build_views: d must be a positive multiple of 8");
-  DAVET_CHECK_ARG(g->dtype == DAVET_F32 || g->dtype == DAVET_BF16, DAVET_EDTYPE,
-                  "davet_build_views: dtype must be DAVET_F32 or DAVET_BF16");
+  DAVET_CHECK_ARG(g->dtype == DAVET_F32 || g->dtype == DAVET_BF16 ||
+                      g->dtype == DAVET_F16, DAVET_EDTYPE,
+                  "davet_build_views: dtype must be DAVET_F32, BF16 or F16");
   DAVET_CHECK_ARG((long long)g->n_crops * g->grid * g->grid < (1ll << 31),
                   DAVET_ESHAPE, "davet_build_views: too many tokens");
   if (g->K > 1) {

@@ -1,11 +1,18 @@
-"""Helpers of the GPU parity tests: device upload of the seeded inputs, the
-oracle-side weight dicts, and the comparison rules.
+"""Helpers of the GPU parity tests: device upload of the seeded inputs in a
+compute mode, the oracle-side values, and the comparison rules.
+
+Compute modes: "f32" (the fp32 configuration), "f16" and "bf16" (16-bit
+matrix-core operands).  A bf16 model runs in either 16-bit mode; in "f16"
+mode its bf16 weights and encodings are converted to fp16 (round to nearest
+even, exact for every value with |x| >= 2^-17) and the oracle is fed the
+very same converted values.
 
 Comparison rules (floating point decides an integer, so the argmax is
 compared where it is unique at the tolerance, and checked for validity
 elsewhere):
   logits   relative RMS error over the masked rows <= tol (1e-5 for the fp32
-           path; 1e-2 for bf16, against the oracle fed the same bf16 values)
+           path; 1e-2 for the 16-bit modes, against the oracle fed the same
+           16-bit values)
   argmax   equal wherever the oracle's top-two gap exceeds ``gap`` (a few
            times the absolute logit error); elsewhere the GPU's choice must be
            within ``gap`` of the oracle's maximum
@@ -17,49 +24,111 @@ import torch
 
 import paper_2608_01821_amd as dv
 import synth
+from oracle import decode, model, views
+
+TOL = {"f32": dict(logits=1e-5, gap=1e-4, conf=1e-4),
+       "bf16": dict(logits=1e-2, gap=None, conf=5e-2),
+       "f16": dict(logits=1e-2, gap=None, conf=5e-2)}
+
+DTYPE = {"f32": dv.DAVET_F32, "bf16": dv.DAVET_BF16, "f16": dv.DAVET_F16}
 
 
-def dev_tensor(arr, cfg_dtype):
-    """float32 numpy array -> device tensor in the model dtype (bf16 bits
-    stored as int16; values already bf16-representable)."""
-    if cfg_dtype == "bf16":
-        bits = synth.f32_to_bf16_bits(np.ascontiguousarray(arr, np.float32))
-        return torch.from_numpy(bits.view(np.int16)).cuda()
-    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
+def default_mode(cfg):
+    return "f32" if cfg.dtype == "f32" else "f16"
 
 
-def model_cfg(cfg):
+def to_mode(arr, mode):
+    """(numpy array stored on the device, float32 values the device sees)."""
+    a = np.ascontiguousarray(arr, np.float32)
+    if mode == "f16":
+        h = a.astype(np.float16)
+        return h.view(np.int16), h.astype(np.float32)
+    if mode == "bf16":
+        bits = synth.f32_to_bf16_bits(a)
+        return bits.view(np.int16), synth.bf16_bits_to_f32(bits)
+    return a, a
+
+
+def dev_tensor(arr, mode):
+    return torch.from_numpy(to_mode(arr, mode)[0]).cuda()
+
+
+def model_cfg(cfg, mode=None):
+    mode = mode or default_mode(cfg)
     return dv.ModelCfg(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn,
                        cfg.vocab, cfg.mask_id, cfg.rms_eps, cfg.rope_theta,
-                       dv.DAVET_BF16 if cfg.dtype == "bf16" else dv.DAVET_F32)
+                       DTYPE[mode])
 
 
-def view_geom(cfg, n_crops):
-    return dv.ViewGeom(n_crops, cfg.grid, cfg.d, cfg.K,
-                       dv.DAVET_BF16 if cfg.dtype == "bf16" else dv.DAVET_F32)
+def view_geom(cfg, n_crops, mode=None):
+    mode = mode or default_mode(cfg)
+    return dv.ViewGeom(n_crops, cfg.grid, cfg.d, cfg.K, DTYPE[mode])
 
 
 class Model:
-    """Seeded weights on both sides: ``host`` feeds the oracle (float32
-    arrays holding the same values), ``dev`` is the library's struct."""
+    """Seeded weights on both sides in one compute mode.  ``host`` feeds the
+    oracle the exact values the device holds -- in memory, or regenerated per
+    layer on demand when ``stream_host`` is set (large stacks)."""
 
-    def __init__(self, cfg, keep_host=True):
+    def __init__(self, cfg, mode=None, keep_host=True, stream_host=False):
         self.cfg = cfg
-        embed = synth.gen_embed(cfg)
-        head = synth.gen_head(cfg)
-        layers = [synth.gen_layer_weights(cfg, i) for i in range(cfg.n_layers)]
-        self.dev_layers = [{k: dev_tensor(v, cfg.dtype) for k, v in lw.items()}
-                           for lw in layers]
-        self.dev_embed = dev_tensor(embed, cfg.dtype)
-        self.dev_head = dev_tensor(head, cfg.dtype)
+        self.mode = mode = mode or default_mode(cfg)
+
+        def both(a):
+            dev, host = to_mode(a, mode)
+            return torch.from_numpy(dev).cuda(), host
+
+        self.dev_layers = []
+        host_layers = []
+        for i in range(cfg.n_layers):
+            lw = synth.gen_layer_weights(cfg, i)
+            pair = {k: both(v) for k, v in lw.items()}
+            del lw
+            self.dev_layers.append({k: p[0] for k, p in pair.items()})
+            if keep_host and not stream_host:
+                host_layers.append({k: p[1] for k, p in pair.items()})
+        self.dev_embed, embed = both(synth.gen_embed(cfg))
+        self.dev_head, head = both(synth.gen_head(cfg))
         self.weights = dv.Weights(self.dev_embed, self.dev_head,
                                   self.dev_layers)
-        self.host = dict(embed=embed, head=head, layers=layers) \
-            if keep_host else None
+        self.host = None
+        if keep_host:
+            if stream_host:
+                def layers(i):
+                    return {k: to_mode(v, mode)[1] for k, v in
+                            synth.gen_layer_weights(cfg, i).items()}
+            else:
+                layers = host_layers
+            self.host = dict(embed=embed, head=head, layers=layers)
 
 
-def workspace(cfg, max_tokens, n_seqs, L):
-    nbytes = dv.davet_workspace_bytes(model_cfg(cfg), max_tokens, n_seqs, L)
+class Sample:
+    """One sample's inputs on both sides and its GPU-built views."""
+
+    def __init__(self, cfg, n_crops, visual, prompt, mode=None):
+        self.cfg = cfg
+        self.mode = mode = mode or default_mode(cfg)
+        dev_v, host_v = to_mode(visual, mode)
+        self.visual = host_v
+        self.prompt = prompt
+        self.n_crops = n_crops
+        self.ref_levels, _ = views.build_views(host_v, n_crops, cfg.grid,
+                                               cfg.K, mode)
+        geom = view_geom(cfg, n_crops, mode)
+        self.sizes = dv.davet_view_sizes(geom)
+        self.dev_v = torch.from_numpy(dev_v).cuda()
+        tdt = torch.float32 if mode == "f32" else torch.int16
+        self.dev_levels = [torch.empty((self.sizes[l], cfg.d), dtype=tdt,
+                                       device="cuda")
+                           for l in range(cfg.K - 1)]
+        dv.davet_build_views(geom, self.dev_v, self.dev_levels)
+        self.dev_levels.append(self.dev_v)
+        self.dev_prompt = torch.from_numpy(prompt).cuda()
+
+
+def workspace(cfg, max_tokens, n_seqs, L, mode=None):
+    nbytes = dv.davet_workspace_bytes(model_cfg(cfg, mode), max_tokens,
+                                      n_seqs, L)
     return torch.empty(nbytes, dtype=torch.uint8, device="cuda")
 
 
@@ -96,3 +165,47 @@ def random_state(rng, L, mask_id, vocab, frac_masked):
     ids = rng.integers(0, vocab - 1, L).astype(np.int32)
     ids[masked == 1] = mask_id
     return ids, masked
+
+
+def run_gpu_step(cfg, mdl, samples, levels, ids, masked, want_logits=True):
+    n = len(samples)
+    L = cfg.resp_len
+    mode = mdl.mode
+    prompt = torch.cat([s.dev_prompt for s in samples])
+    cu = np.concatenate([[0], np.cumsum([len(s.prompt) for s in samples])])
+    views_ = [s.dev_levels[lv] for s, lv in zip(samples, levels)]
+    nview = [s.sizes[lv] for s, lv in zip(samples, levels)]
+    total = sum(nview) + int(cu[-1]) + n * L
+    ws = workspace(cfg, total, n, L, mode)
+    d_ids = torch.from_numpy(np.ascontiguousarray(ids, np.int32)).cuda()
+    d_m = torch.from_numpy(np.ascontiguousarray(masked, np.uint8)).cuda()
+    conf = torch.full((n * L,), 123.0, device="cuda")
+    am = torch.full((n * L,), -7, dtype=torch.int32, device="cuda")
+    logits = torch.full((n * L, cfg.vocab), 55.0, device="cuda") \
+        if want_logits else None
+    dv.davet_denoise_step(model_cfg(cfg, mode), mdl.weights, views_, nview,
+                          prompt, cu, d_ids, d_m, L, conf, am, logits, ws)
+    torch.cuda.synchronize()
+    return (conf.cpu().numpy().reshape(n, L), am.cpu().numpy().reshape(n, L),
+            None if logits is None else
+            logits.cpu().numpy().reshape(n, L, cfg.vocab))
+
+
+def oracle_step(cfg, mdl, sample, level, ids, masked, rows=None):
+    pos, lg = model.step_logits(cfg, sample.ref_levels[level], sample.prompt,
+                                ids, masked, mdl.host, rows=rows)
+    am, cf = decode.argmax_conf(lg, cfg.mask_id)
+    return pos, lg, am, cf
+
+
+def compare(cfg, tol, masked, g_conf, g_am, g_logits, pos, ref_lg, ref_am,
+            ref_cf):
+    m = masked.astype(bool)
+    assert np.all(g_conf[~m] == -np.inf) and np.all(g_am[~m] == -1)
+    err = rel_rms(g_logits[pos], ref_lg)
+    assert err <= tol["logits"], ("logits rel-RMS", err)
+    assert np.all(g_logits[~m] == 55.0)            # only masked rows written
+    gap = tol["gap"] or 6.0 * err * float(np.sqrt(np.mean(ref_lg ** 2)))
+    check_decode(g_am[pos], g_conf[pos], ref_lg, ref_am, ref_cf, cfg.mask_id,
+                 gap, tol["conf"])
+    return err

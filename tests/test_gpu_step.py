@@ -11,90 +11,22 @@ import numpy as np
 import pytest
 import torch
 
-import paper_2608_01821_amd as dv
 import synth
-from oracle import decode, model, views
-from gpu_util import (Model, check_decode, dev_tensor, model_cfg, random_state,
-                      rel_rms, view_geom, workspace)
+from gpu_util import (TOL, Model, Sample, compare, oracle_step, random_state,
+                      run_gpu_step)
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"f32": dict(logits=1e-5, gap=1e-4, conf=1e-4),
-       "bf16": dict(logits=1e-2, gap=None, conf=5e-2)}
 
-
-class Sample:
-    """One sample's inputs on both sides and its GPU-built views."""
-
-    def __init__(self, cfg, n_crops, visual, prompt):
-        self.cfg = cfg
-        self.visual = visual
-        self.prompt = prompt
-        self.n_crops = n_crops
-        self.ref_levels, _ = views.build_views(visual, n_crops, cfg.grid,
-                                               cfg.K, cfg.dtype)
-        geom = view_geom(cfg, n_crops)
-        self.sizes = dv.davet_view_sizes(geom)
-        self.dev_v = dev_tensor(visual, cfg.dtype)
-        tdt = torch.int16 if cfg.dtype == "bf16" else torch.float32
-        self.dev_levels = [torch.empty((self.sizes[l], cfg.d), dtype=tdt,
-                                       device="cuda")
-                           for l in range(cfg.K - 1)]
-        dv.davet_build_views(geom, self.dev_v, self.dev_levels)
-        self.dev_levels.append(self.dev_v)
-        self.dev_prompt = torch.from_numpy(prompt).cuda()
-
-
-def run_gpu_step(cfg, mdl, samples, levels, ids, masked, want_logits=True):
-    n = len(samples)
-    L = cfg.resp_len
-    prompt = torch.cat([s.dev_prompt for s in samples])
-    cu = np.concatenate([[0], np.cumsum([len(s.prompt) for s in samples])])
-    views_ = [s.dev_levels[lv] for s, lv in zip(samples, levels)]
-    nview = [s.sizes[lv] for s, lv in zip(samples, levels)]
-    total = sum(nview) + int(cu[-1]) + n * L
-    ws = workspace(cfg, total, n, L)
-    d_ids = torch.from_numpy(np.ascontiguousarray(ids, np.int32)).cuda()
-    d_m = torch.from_numpy(np.ascontiguousarray(masked, np.uint8)).cuda()
-    conf = torch.full((n * L,), 123.0, device="cuda")
-    am = torch.full((n * L,), -7, dtype=torch.int32, device="cuda")
-    logits = torch.full((n * L, cfg.vocab), 55.0, device="cuda") \
-        if want_logits else None
-    dv.davet_denoise_step(model_cfg(cfg), mdl.weights, views_, nview, prompt,
-                          cu, d_ids, d_m, L, conf, am, logits, ws)
-    torch.cuda.synchronize()
-    return (conf.cpu().numpy().reshape(n, L), am.cpu().numpy().reshape(n, L),
-            None if logits is None else
-            logits.cpu().numpy().reshape(n, L, cfg.vocab))
-
-
-def oracle_step(cfg, mdl, sample, level, ids, masked, rows=None):
-    pos, lg = model.step_logits(cfg, sample.ref_levels[level], sample.prompt,
-                                ids, masked, mdl.host, rows=rows)
-    am, cf = decode.argmax_conf(lg, cfg.mask_id)
-    return pos, lg, am, cf
-
-
-def compare(cfg, tol, masked, g_conf, g_am, g_logits, pos, ref_lg, ref_am,
-            ref_cf):
-    m = masked.astype(bool)
-    assert np.all(g_conf[~m] == -np.inf) and np.all(g_am[~m] == -1)
-    err = rel_rms(g_logits[pos], ref_lg)
-    assert err <= tol["logits"], ("logits rel-RMS", err)
-    if g_logits is not None:
-        assert np.all(g_logits[~m] == 55.0)        # only masked rows written
-    gap = tol["gap"] or 6.0 * err * float(np.sqrt(np.mean(ref_lg ** 2)))
-    check_decode(g_am[pos], g_conf[pos], ref_lg, ref_am, ref_cf, cfg.mask_id,
-                 gap, tol["conf"])
-    return err
-
-
-@pytest.fixture(scope="module", params=[1, 11])
+@pytest.fixture(scope="module", params=[(1, "f32"), (11, "f16"),
+                                        (11, "bf16")])
 def small(request):
-    cfg = synth.get_any_config(request.param)
-    mdl = Model(cfg)
+    cid, mode = request.param
+    cfg = synth.get_any_config(cid)
+    mdl = Model(cfg, mode)
     s = synth.gen_sample(cfg)
-    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0])
+    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0],
+                    mode)
     return cfg, mdl, sample
 
 
@@ -106,7 +38,7 @@ def test_step_teacher_forced_small(small, level, frac):
     ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, frac)
     g_conf, g_am, g_lg = run_gpu_step(cfg, mdl, [sample], [level], ids, masked)
     pos, lg, am, cf = oracle_step(cfg, mdl, sample, level, ids, masked)
-    compare(cfg, TOL[cfg.dtype], masked, g_conf[0], g_am[0], g_lg[0], pos, lg,
+    compare(cfg, TOL[mdl.mode], masked, g_conf[0], g_am[0], g_lg[0], pos, lg,
             am, cf)
 
 
@@ -120,15 +52,15 @@ def test_step_deterministic(small):
         assert np.array_equal(x, y, equal_nan=True)
 
 
-@pytest.mark.parametrize("cid", [12, 13])
-def test_ragged_batch_step(cid):
+@pytest.mark.parametrize("cid,mode", [(12, "f16"), (12, "bf16"), (13, "f32")])
+def test_ragged_batch_step(cid, mode):
     """Packed batch of sequences with different view levels and prompt
     lengths in one call; each sequence must equal its own oracle run (the
     attention of one sequence never sees another's tokens)."""
     cfg = synth.get_any_config(cid)
-    mdl = Model(cfg)
+    mdl = Model(cfg, mode)
     s = synth.gen_sample(cfg)
-    samples = [Sample(cfg, c, v, p) for c, v, p in
+    samples = [Sample(cfg, c, v, p, mode) for c, v, p in
                zip(s["n_crops"], s["visual"], s["prompts"])]
     rng = np.random.default_rng(cid)
     levels = [int(x) for x in rng.integers(0, cfg.K, len(samples))]
@@ -139,5 +71,5 @@ def test_ragged_batch_step(cid):
     for i, smp in enumerate(samples):
         pos, lg, am, cf = oracle_step(cfg, mdl, smp, levels[i], ids[i],
                                       masked[i])
-        compare(cfg, TOL[cfg.dtype], masked[i], g_conf[i], g_am[i], g_lg[i],
+        compare(cfg, TOL[mode], masked[i], g_conf[i], g_am[i], g_lg[i],
                 pos, lg, am, cf)

@@ -9,7 +9,7 @@ import torch
 import paper_2608_01821_amd as dv
 import synth
 from oracle import decode, views
-from gpu_util import dev_tensor
+from gpu_util import DTYPE, dev_tensor, to_mode
 
 pytestmark = pytest.mark.gpu
 
@@ -22,17 +22,20 @@ pytestmark = pytest.mark.gpu
     ("bf16", 3, 5, 2, 16),        # two levels
     ("f32", 1, 1, 3, 8),          # a single token
     ("bf16", 2, 13, 1, 24),       # one level: nothing pooled, identity map
+    ("f16", 1, 27, 3, 4096),      # fp16 operand mode
+    ("f16", 4, 27, 3, 4096),      # four crops: 2916 -> 784 -> 196
+    ("f16", 2, 7, 4, 64),
 ])
 def test_views_match_oracle(dtype, C, G, K, d):
     rng = np.random.default_rng(100 + C * 7 + G + K)
     v = rng.standard_normal((C * G * G, d)).astype(np.float32)
     if dtype == "bf16":
         v = synth.round_to_bf16(v)
+    v = to_mode(v, dtype)[1]
     vd = dev_tensor(v, dtype)
-    geom = dv.ViewGeom(C, G, d, K, dv.DAVET_BF16 if dtype == "bf16"
-                       else dv.DAVET_F32)
+    geom = dv.ViewGeom(C, G, d, K, DTYPE[dtype])
     sizes = dv.davet_view_sizes(geom)
-    tdt = torch.int16 if dtype == "bf16" else torch.float32
+    tdt = torch.float32 if dtype == "f32" else torch.int16
     levels = [torch.full((sizes[l], d), -7, dtype=tdt, device="cuda")
               for l in range(K - 1)]
     offs = [torch.full((sizes[l] + 1,), -1, dtype=torch.int32, device="cuda")
@@ -47,8 +50,9 @@ def test_views_match_oracle(dtype, C, G, K, d):
         assert np.array_equal(mems[l].cpu().numpy(), ref_maps[l][1])
     for l in range(K - 1):
         got = levels[l].cpu().numpy()
-        if dtype == "bf16":
-            got = synth.bf16_bits_to_f32(got.view(np.uint16))
+        if dtype != "f32":
+            got = synth.bf16_bits_to_f32(got.view(np.uint16)) \
+                if dtype == "bf16" else got.view(np.float16).astype(np.float32)
             assert np.array_equal(got, ref_levels[l])      # bit-exact
         else:
             ref = ref_levels[l]
@@ -113,3 +117,26 @@ def test_unmask_reveals_everything_after_enough_steps():
     assert counts == [6, 6, 6, 6, 6, 6, 4]
     assert int(d_m.sum()) == 0
     assert np.array_equal(d_ids.cpu().numpy()[0], np.arange(L))
+
+
+@pytest.mark.parametrize("src,dst", [("bf16", "f16"), ("f32", "f16"),
+                                     ("f32", "bf16"), ("f16", "f32")])
+def test_convert_matches_numpy(src, dst):
+    """davet_convert rounds to nearest even exactly as numpy does, including
+    fp16 subnormals, overflow to infinity and tiny bf16 values."""
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(100003) *
+         np.exp(rng.uniform(-20, 12, 100003))).astype(np.float32)
+    x[:4] = [0.0, -0.0, 70000.0, 2.0 ** -26]
+    if src == "bf16":
+        x = synth.round_to_bf16(x)
+    elif src == "f16":
+        x = x.astype(np.float16).astype(np.float32)
+    d_src = dev_tensor(x, src)
+    tdt = torch.float32 if dst == "f32" else torch.int16
+    d_dst = torch.empty(x.size, dtype=tdt, device="cuda")
+    dv.davet_convert(d_src, DTYPE[src], d_dst, DTYPE[dst])
+    torch.cuda.synchronize()
+    got = d_dst.cpu().numpy()
+    exp = to_mode(x, dst)[0]
+    assert np.array_equal(got.view(np.uint8), exp.view(np.uint8))

@@ -121,3 +121,33 @@ def test_bf16_single_rounding_from_double():
     got = views._round_f64_to_bf16(xs)
     exp = np.array([_nearest_bf16(float(x)) for x in xs], dtype=np.float32)
     np.testing.assert_array_equal(got, exp)
+
+
+def _nearest_f16(x: float) -> float:
+    """Nearest binary16 to x by exact rational comparison, ties to even."""
+    h = np.float16(np.float32(x))       # a neighbour within one step
+    bits = int(np.array([h]).view(np.uint16)[0])
+    cands = []
+    for b in (bits - 1, bits, bits + 1):
+        if not 0 <= b <= 0xFFFF:
+            continue
+        val = np.array([b], dtype=np.uint16).view(np.float16)[0]
+        if not np.isfinite(val):
+            continue
+        cands.append((abs(Fraction(float(val)) - Fraction(x)), b & 1,
+                      float(val)))
+    cands.sort()
+    return cands[0][2]
+
+
+def test_f16_single_rounding_from_double():
+    """fp16 views: float64 means round once to binary16 (subnormals too)."""
+    rng = np.random.default_rng(6)
+    xs = rng.standard_normal(3000) * np.exp(rng.uniform(-14, 6, 3000))
+    ties = [1.0 + 2 ** -11, 1.0 + 3 * 2 ** -11, 2.0 ** -20 + 2.0 ** -25,
+            1.0 + 2 ** -11 + 2 ** -40, -(1.0 + 2 ** -11)]
+    xs = np.concatenate([xs, ties])
+    # one-token windows (grid 1, K = 1): each "mean" is the value itself
+    got = views.pool_level(xs.reshape(-1, 1), len(xs), 1, 1, 0, "f16")[:, 0]
+    exp = np.array([_nearest_f16(float(x)) for x in xs], dtype=np.float32)
+    np.testing.assert_array_equal(got, exp)
