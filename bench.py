@@ -57,7 +57,27 @@ def parse():
     ap.add_argument("--mode", choices=["f16", "bf16"], default="f16",
                     help="16-bit operand format for a bf16 model (f16: its "
                          "weights converted exactly; default)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only stream MIB MiB of fp32 through a plain "
+                         "elementwise copy (y = x * 1) five times and exit: "
+                         "the known-size reference for HBM byte counters")
     return ap.parse_args()
+
+
+def copy_calibration(mib):
+    """Five launches of a plain copy of known size: each reads and writes
+    exactly ``mib`` MiB, so byte counters read on it give the scale factor
+    between counter units and bytes."""
+    import torch
+    n = (mib << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4,
+                      "copy_calibration_bytes_written": n * 4,
+                      "launches": 5}), flush=True)
 
 
 def setup(cfg, mode):
@@ -177,32 +197,67 @@ def work_per_loop(cfg, st, levels):
     return w, total_flops
 
 
-def roofline(cfg, kern, work, loops):
-    """Roofline object of the kernel class that took the most time."""
-    mm = {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o",
-          "gemm_gateup": "gemm_gateup", "gemm_down": "gemm_down",
-          "attention": "attention", "gemm_f32": None, "attention_f32": None}
-    ranked = sorted(kern.items(), key=lambda kv: -kv[1][1])
-    for name, (cnt, ms) in ranked:
-        if cnt == 0:
-            continue
-        sec = ms / 1e3
-        if name in mm and mm[name]:
-            flops = work[mm[name]] * loops
-            peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
-            ach = flops / sec / 1e12
-            return dict(kernel=name, bound="mfma", achieved=round(ach, 2),
-                        peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
-                        traffic=None, launches=cnt,
-                        mean_launch_us=round(ms * 1e3 / cnt, 2))
-        if name == "head_gemm":
-            byts = work["head_gemm_bytes"] * loops
-            ach = byts / sec / 1e9
-            return dict(kernel=name, bound="hbm", achieved=round(ach, 1),
-                        peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=None,
-                        launches=cnt, mean_launch_us=round(ms * 1e3 / cnt, 2))
-    return None
+MATRIX_CLASSES = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down",
+                  "attention")
+ROOFLINE_CLASSES = MATRIX_CLASSES + ("head_gemm",)
+
+
+def dominant_class(kern):
+    """The kernel class (with an algorithmic-work model) that took the most
+    time in a profiled pass."""
+    ranked = sorted(((ms, name) for name, (cnt, ms) in kern.items()
+                     if cnt and name in ROOFLINE_CLASSES), reverse=True)
+    return ranked[0][1] if ranked else None
+
+
+def measured_traffic(name, workload):
+    """HBM bytes per launch of a kernel class, as measured by the FETCH_SIZE
+    and WRITE_SIZE counters and scaled by a plain copy kernel's readings
+    (profiles/<class>_<workload>.md).  None unless the kernel sources are
+    byte-identical to those the counters were taken on."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "%s_%s.md" % (name, workload))
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                fields[k.strip("`")] = v.strip().strip("`")
+    try:
+        for src, want in zip(fields["sources"].split(","),
+                             fields["sources_sha256"].split(",")):
+            with open(os.path.join(ROOT, src.strip()), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest()[:16] != want.strip():
+                    return None
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, OSError, ValueError):
+        return None
+
+
+def roofline(cfg, name, cnt, ms, work, loops):
+    """Roofline object of one kernel class from its timed launches."""
+    if not name or cnt == 0:
+        return None
+    sec = ms / 1e3
+    traffic = measured_traffic(name, cfg.name)
+    if name in MATRIX_CLASSES:
+        flops = work[name] * loops
+        peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
+        ach = flops / sec / 1e12
+        return dict(kernel=name, bound="mfma", achieved=round(ach, 2),
+                    peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
+                    traffic=traffic, traffic_unit="HBM bytes per launch",
+                    launches=cnt, mean_launch_us=round(ms * 1e3 / cnt, 2))
+    byts = work["head_gemm_bytes"] * loops
+    ach = byts / sec / 1e9
+    return dict(kernel=name, bound="hbm", achieved=round(ach, 1),
+                peak=PEAK_HBM_GBS, unit="GB/s",
+                frac=round(ach / PEAK_HBM_GBS, 4), traffic=traffic,
+                traffic_unit="HBM bytes per launch",
+                algorithmic_bytes_per_launch=round(byts / cnt),
+                launches=cnt, mean_launch_us=round(ms * 1e3 / cnt, 2))
 
 
 def cpu_baseline(cfg, st, n_layers_run):
@@ -271,6 +326,9 @@ def main():
               "path (requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world),
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import torch
     import synth
 
@@ -282,30 +340,42 @@ def main():
         run_loop(cfg, st)
     torch.cuda.synchronize()
 
-    levels, _ = run_loop(cfg, st)          # schedule actually taken
+    # one untimed pass with events around every launch: the schedule taken,
+    # the per-class breakdown and the dominant kernel class
+    per_loop = cfg.steps * (12 * cfg.n_layers + 16) + 64
+    if not args.no_kernel_timing:
+        dv.prof_enable(per_loop)
+    levels, _ = run_loop(cfg, st)
     torch.cuda.synchronize()
+    kern = {}
+    if not args.no_kernel_timing:
+        kern = dv.prof_read()
+        dv.prof_enable(0)
     st["levels"] = levels
     work, flops_loop = work_per_loop(cfg, st, levels)
+    dom = dominant_class(kern)
 
-    if not args.no_kernel_timing:
-        launches = args.steps * cfg.steps * (12 * cfg.n_layers + 16) + 64
-        dv.prof_enable(launches)
+    # timed region: events only around the dominant class's launches
+    if dom:
+        dv.prof_enable(args.steps * per_loop)
+        dv.prof_only(dom)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         run_loop(cfg, st)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    kern = {}
-    if not args.no_kernel_timing:
-        kern = dv.prof_read()
+    rl = None
+    if dom:
+        cnt, ms = dv.prof_read()[dom]
+        dv.prof_only(None)
         dv.prof_enable(0)
+        rl = roofline(cfg, dom, cnt, ms, work, args.steps)
     elapsed = t1 - t0
     loops = args.steps
     steps_per_s = loops * cfg.steps / elapsed
     ms_loop = elapsed / loops * 1e3
 
-    rl = roofline(cfg, kern, work, loops) if kern else None
     kernels = {k: dict(launches=c, total_ms=round(ms, 3),
                        mean_us=round(ms * 1e3 / c, 2) if c else 0.0)
                for k, (c, ms) in kern.items() if c}
@@ -354,7 +424,7 @@ def main():
         "ms_per_denoise_step": round(ms_loop / cfg.steps, 4),
         "tflops_algorithmic": round(flops_loop * loops / elapsed / 1e12, 2),
         "roofline": rl,
-        "kernels": kernels,
+        "kernels_untimed_pass": kernels,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

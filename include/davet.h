@@ -288,9 +288,12 @@ int davet_run_schedule(const davet_model_cfg* cfg, const davet_weights* w,
  * and releases them.  davet_prof_read synchronises on the recorded events and
  * fills, per kernel class c < n_classes, the launch count and summed
  * milliseconds; names via davet_prof_class_name.  Returns the number of
- * classes, or a negative status. */
+ * classes, or a negative status.  davet_prof_only(c) restricts recording to
+ * launches of class c (so that a timed run carries events around one kernel
+ * class only); -1 records every class again. */
 int davet_prof_enable(int32_t max_launches);
 int davet_prof_reset(void);
+int davet_prof_only(int32_t cls);
 int davet_prof_read(int32_t n_classes, int64_t* counts /*host*/,
                     double* total_ms /*host*/);
 const char* davet_prof_class_name(int32_t cls);

@@ -99,6 +99,7 @@ _SIGS = {
                                      C.c_size_t, _vp]),
     "davet_prof_enable": (C.c_int, [_i32]),
     "davet_prof_reset": (C.c_int, []),
+    "davet_prof_only": (C.c_int, [_i32]),
     "davet_prof_read": (C.c_int, [_i32, _P_i64, _P_f64]),
     "davet_prof_class_name": (C.c_char_p, [_i32]),
 }
@@ -290,6 +291,22 @@ def prof_enable(max_launches):
 
 def prof_reset():
     _check(_L.davet_prof_reset())
+
+
+def prof_only(cls_name=None):
+    """Record only launches of the named kernel class (None: every class)."""
+    idx = -1
+    if cls_name is not None:
+        i = 0
+        while True:
+            n = _L.davet_prof_class_name(i)
+            if not n:
+                raise DavetError(-1, "unknown kernel class %r" % cls_name)
+            if n.decode() == cls_name:
+                idx = i
+                break
+            i += 1
+    _check(_L.davet_prof_only(idx))
 
 
 def prof_read():

@@ -159,7 +159,8 @@ int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const void* embed, const int32_t* prompt_ids,
                          const int32_t* resp_ids, const uint8_t* masked,
                          int mask_id, int vocab, int d, const float* gain,
-                         float eps, float* X, void* A, hipStream_t s);
+                         float eps, float* X, void* A, int32_t* pos,
+                         hipStream_t s);
 int launch_rmsnorm(const float* X, int rows, int d, const float* gain,
                    float eps, int dtype, void* A, hipStream_t s);
 int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
@@ -182,13 +183,36 @@ int launch_head_reduce_f32(const float* logits, const int32_t* list,
 
 // GEMMs: C[M,N] = A[M,K] * B[N,K]^T
 enum Epilogue { EPI_STORE = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
-int launch_gemm16(int dtype, int epi, const uint16_t* A, const uint16_t* B,
-                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
-                  int cls, hipStream_t s);
+struct GemmPlan {
+  int tile;      // kernel variant (tile shape, K slab, stages, waves)
+  int ksplit;    // > 1: fp32 partials [ksplit][M][N] + a reduction kernel
+};
+// Tile shape and K split for an M x N x K product (N = 2*ffn for SwiGLU).
+GemmPlan plan_gemm16(int M, int N, int K);
+// 16-bit GEMM with fused epilogue.  EPI_STORE applies the rotary embedding to
+// columns < rope_cols using pos[row] and the cos/sin table cs when pos is
+// given.  With plan.ksplit > 1 the kernel writes fp32 partials to `partials`
+// and the caller runs the matching reduce kernel below.
+int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
+                  const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
+                  int K, int ldc, const int32_t* pos, const float* cs,
+                  int rope_cols, float* partials, int cls, hipStream_t s);
+// Split-K reductions (fixed summation order over the splits):
+//   X[r] += sum_s P[s][r]; then A[r] = RMSNorm(X[r]) * gain when A is given
+int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,
+                           int d, float* X, const float* gain, float eps,
+                           void* A, hipStream_t s);
+//   out16[r][c] = rope(sum_s P[s][r][c]) for c < rope_cols, plain otherwise
+int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
+                             int ncols, int rope_cols, const int32_t* pos,
+                             const float* cs, void* out, hipStream_t s);
+//   out16[r][c] = silu(sum_s P[s][r][c]) * sum_s P[s][r][F + c]
+int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
+                         int ffn, void* out, hipStream_t s);
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s);
+                  float* logits_out, hipStream_t s, int variant = -1);
 int head16_slabs(int vocab);
 int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     float* C, int M, int N, int K, int ldc, int cls,

@@ -1,44 +1,72 @@
-// 16-bit (bf16 or fp16) matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] * B[N,K]^T with both
-// operands K-contiguous (activations row-major, weights [out, in]).
+// 16-bit (fp16 or bf16) matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] B[N,K]^T
+// with both operands K-contiguous (activations row-major, weights [out, in]).
 //
-// Tiling for CDNA4: a 256-thread workgroup (4 wavefronts, 2 x 2) owns a
-// BM x BN output tile; each wavefront issues v_mfma_f32_32x32x16_bf16 on a
-// (BM/2) x (BN/2) sub-tile.  K advances in slabs of 64 staged through LDS with
-// double buffering (global loads of slab k+1 are in flight while slab k feeds
-// the matrix cores; one barrier per slab).  LDS rows are padded by 16 bytes so
-// the 16-byte fragment reads of a half-wavefront hit distinct banks.
-// Workgroup ids are remapped so each XCD (ids congruent mod 8) walks a
-// contiguous run of tiles with the M index fastest: a weight tile is fetched
-// into one XCD's L2 and reused by every M tile of that column.
+// CDNA4 design.  A 256-thread workgroup (2 x 2 wavefronts) owns a BM x BN
+// tile; each wavefront issues v_mfma_f32_32x32x16 on (BM/2) x (BN/2).  K moves
+// in slabs of 32 through a 4-deep ring of LDS stages filled by direct
+// global->LDS loads (global_load_lds_dwordx4: no VGPR staging), so up to three
+// slabs are in flight while one feeds the matrix cores; one barrier per slab.
+// Each LDS row is 64 bytes (4 chunks of 16 B); chunk c of row r sits in slot
+// c ^ ((r >> 2) & 3), which spreads the 16-byte fragment reads of 16
+// consecutive rows over distinct bank groups.  Workgroup ids are remapped so
+// each XCD (ids congruent mod 8) walks a contiguous run of tiles, M fastest:
+// a weight tile is fetched into one XCD's L2 and reused by every M tile.
 //
-// Epilogues (fused, no extra pass over C):
-//   EPI_STORE    C (16-bit) = acc
-//   EPI_ADD_F32  C f32 += acc           (residual stream update)
-//   EPI_SWIGLU   dual weight: the tile's first BN/2 columns come from B (gate),
-//                the last BN/2 from B2 (up) at the same output index; the wave
-//                layout puts gate and up of one column in the same lane, so
-//                C (16-bit) = silu(gate) * up is formed in registers.
-//   head         vocabulary slab reduction: per row, (max, first argmax, sum of
-//                exp(l - max)) over the slab's columns with [MASK] excluded.
+// Split-K: with few output tiles (short sequences) the K range is cut into
+// ksplit parts whose fp32 partial tiles land in a workspace; a row kernel
+// sums them in a fixed order (deterministic) and applies the epilogue.
+//
+// Epilogues, fused:
+//   EPI_STORE    16-bit C = acc, with the rotary embedding applied in fp32 to
+//                the query/key columns (a lane owns dims i and i+64 of a head)
+//   EPI_ADD_F32  fp32 C += acc (residual stream)
+//   EPI_SWIGLU   B holds gate rows, B2 up rows; gate and up of one output
+//                column sit in the same lane: 16-bit C = silu(gate) * up
+//   EPI_HEAD     vocabulary slab reduction per row: (max, first argmax,
+//                sum exp(l - max)) with [MASK] excluded
+//   EPI_PARTIAL  fp32 partial tile of one K split
+
+#include <algorithm>
 
 #include "common.h"
 
 namespace davet {
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDS_STRIDE = BK + 8;     // elements; 144-byte rows
+constexpr int BK_MIN = 32;   // K must be a multiple of this
 constexpr int EPI_HEAD = 3;
 
-struct HeadArgs {
-  const int32_t* list;   // list[0] = live rows, list[1+j] = global position
-  int vocab;
-  int mask_id;
-  int n_slabs;
+// Kernel variants: tile BM x BN, K slab BK (64-byte or 128-byte LDS rows),
+// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2 grid).
+template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_>
+struct Var {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_,
+                       WAVES = WAVES_;
+  static constexpr int LDS = STAGES * (BM + BN) * BK * 2;
+  // workgroups per CU the register budget must allow (LDS is 160 KB per CU)
+  static constexpr int MINB = LDS <= 80 * 1024 ? (LDS <= 53 * 1024 ? 3 : 2) : 1;
+};
+constexpr int EPI_PARTIAL = 4;
+
+struct EpiArgs {
+  void* C;
+  int ldc;
+  // rotary embedding (EPI_STORE): columns < rope_cols are rotated
+  const int32_t* pos;
+  const float2* cs;
+  int rope_cols;
+  // vocabulary head
+  const int32_t* list;
+  int vocab, mask_id, n_slabs;
   float* pmax;
   float* psum;
   int32_t* parg;
-  float* logits_out;     // nullable
+  float* logits_out;
+  // split-K partials: part[ks][row][col], row stride part_ld
+  float* part;
+  int part_ld;
+  int dual;              // B/B2 gate/up weights (SwiGLU), also for partials
+  int ffn;
 };
 
 __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
@@ -48,57 +76,121 @@ __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
   return (bid & 7) * per + (bid >> 3);
 }
 
-template <typename Fmt, int BM, int BN, int EPI>
-__global__ void __launch_bounds__(256, 1)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without the memory fence __syncthreads() carries: the
+// fence would wait for every outstanding global->LDS load (vmcnt(0)) and
+// drain the pipeline.  Each wave has already waited for the slab it needs;
+// the empty asm statements keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)lds, 16, 0, 0);
+}
+
+// Byte offset of chunk c (16 B) of row r inside a stage of BK-wide rows.
+// Slot = c ^ f(r) with f chosen so 16 consecutive rows at the same chunk fall
+// in 16 distinct 16-byte bank groups of a 256-byte bank line.
+template <int BK>
+__device__ __forceinline__ int swz(int r, int c) {
+  constexpr int CPR = BK / 8;                 // 16-byte chunks per row
+  constexpr int RPL = 16 / CPR;               // rows per 256-byte bank line
+  return r * (BK * 2) + ((c ^ ((r / RPL) % CPR)) << 4);
+}
+
+template <typename Fmt, typename V, int EPI>
+__global__ void __launch_bounds__(64 * V::WAVES, V::MINB)
 gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
-                 const uint16_t* __restrict__ B2, void* __restrict__ C, int M,
-                 int N, int K, int ldc, int n_mtiles, HeadArgs ha) {
-  constexpr int TM = BM / 64;            // 32-row sub-tiles per wave
+              const uint16_t* __restrict__ B2, int M, int N, int K,
+              int n_mtiles, int n_ntiles, int ksplit, EpiArgs ep) {
+  using v8 = typename Fmt::v8;
+  constexpr int BM = V::BM, BN = V::BN, BK = V::BK, STAGES = V::STAGES;
+  constexpr int WAVES = V::WAVES;
+  constexpr int WM = WAVES / 2;          // wave grid WM x 2
+  constexpr int WROWS = BM / WM;         // rows per wave
+  constexpr int TM = WROWS / 32;         // 32-row sub-tiles per wave
   constexpr int TN = BN / 64;            // 32-col sub-tiles per wave
-  constexpr int A_LD = BM / 32;          // 16-byte loads per thread
-  constexpr int B_LD = BN / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDS_STRIDE];
+  constexpr int CPR = BK / 8;            // 16-byte chunks per LDS row
+  constexpr int RPI = 64 / CPR;          // rows per load instruction
+  constexpr int AI = BM / (RPI * WAVES); // A load instructions per wave/stage
+  constexpr int BI = BN / (RPI * WAVES); // B load instructions per wave/stage
+  static_assert(AI >= 1 && BI >= 1 && TM >= 1, "tile too small for the waves");
+  constexpr int LPT = AI + BI;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int S_BYTES = A_BYTES + B_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * S_BYTES];
 
   const int nwg = gridDim.x;
   const int tile = remap_xcd(blockIdx.x, nwg);
   const int mb = tile % n_mtiles;
-  const int nb = tile / n_mtiles;
+  const int rest = tile / n_mtiles;
+  const int ks = rest % ksplit;
+  const int nb = rest / ksplit;
   int m_live = M;
-  if constexpr (EPI == EPI_HEAD) m_live = ha.list[0];
-  const int m0 = mb * BM;
-  if (m0 >= m_live) return;
+  if constexpr (EPI == EPI_HEAD) m_live = ep.list[0];
   const int n0 = nb * BN;
+  // M tiles mb, mb + n_mtiles, ... (one tile unless the grid is narrower
+  // than the rows: the vocabulary head sizes it for the live rows)
+  for (int mt = mb; mt * BM < m_live; mt += n_mtiles) {
+  const int m0 = mt * BM;
+  if (mt != mb) __syncthreads();      // LDS of the previous tile retired
+  const int nk_all = K / BK;
+  const int chunk = (nk_all + ksplit - 1) / ksplit;
+  const int kt0 = ks * chunk;
+  const int nk = min(nk_all, kt0 + chunk) - kt0;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const bool dual = (EPI == EPI_SWIGLU) || (EPI == EPI_PARTIAL && ep.dual);
 
-  // global source pointers of this thread's 16-byte chunks
-  const uint16_t* a_src[A_LD];
-  const uint16_t* b_src[B_LD];
+  // ---- per-lane sources of this wave's load instructions (fixed over K)
+  const uint16_t* a_src[AI];
+  const uint16_t* b_src[BI];
 #pragma unroll
-  for (int q = 0; q < A_LD; ++q) {
-    const int r = q * 32 + (t >> 3);
+  for (int q = 0; q < AI; ++q) {
+    const int r = (wave * AI + q) * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ ((r / (16 / CPR)) % CPR);
     const int gm = min(m0 + r, m_live - 1);
-    a_src[q] = A + (size_t)gm * K + (t & 7) * 8;
+    a_src[q] = A + (size_t)gm * K + (size_t)kt0 * BK + c * 8;
   }
 #pragma unroll
-  for (int q = 0; q < B_LD; ++q) {
-    const int r = q * 32 + (t >> 3);
-    const uint16_t* base;
+  for (int q = 0; q < BI; ++q) {
+    const int r = (wave * BI + q) * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ ((r / (16 / CPR)) % CPR);
+    const uint16_t* base = B;
     int gn;
-    if constexpr (EPI == EPI_SWIGLU) {
+    if (dual) {
       const int half = BN / 2;
       base = r < half ? B : B2;
       gn = nb * half + (r < half ? r : r - half);
     } else {
-      base = B;
       gn = min(n0 + r, N - 1);
     }
-    b_src[q] = base + (size_t)gn * K + (t & 7) * 8;
+    b_src[q] = base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
   }
+
+  auto issue = [&](int stage, int kt) {
+    char* sa = smem + stage * S_BYTES;
+    char* sb = sa + A_BYTES;
+#pragma unroll
+    for (int q = 0; q < AI; ++q)
+      dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
+#pragma unroll
+    for (int q = 0; q < BI; ++q)
+      dma16(b_src[q] + (size_t)kt * BK, sb + (wave * BI + q) * 1024);
+  };
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -108,103 +200,126 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  u32x4 ra[A_LD], rb[B_LD];
-  auto gload = [&](int k0) {
+  // 32-row sub-tiles of this wave that hold live rows (wave-uniform)
+  bool live[TM];
 #pragma unroll
-    for (int q = 0; q < A_LD; ++q)
-      ra[q] = *reinterpret_cast<const u32x4*>(a_src[q] + k0);
-#pragma unroll
-    for (int q = 0; q < B_LD; ++q)
-      rb[q] = *reinterpret_cast<const u32x4*>(b_src[q] + k0);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < A_LD; ++q)
-      *reinterpret_cast<u32x4*>(&As[buf][(q * 32 + (t >> 3)) * LDS_STRIDE +
-                                         (t & 7) * 8]) = ra[q];
-#pragma unroll
-    for (int q = 0; q < B_LD; ++q)
-      *reinterpret_cast<u32x4*>(&Bs[buf][(q * 32 + (t >> 3)) * LDS_STRIDE +
-                                         (t & 7) * 8]) = rb[q];
-  };
+  for (int i = 0; i < TM; ++i) live[i] = m0 + wm * WROWS + i * 32 < m_live;
 
-  const int nk = K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int lr = lane & 31;           // row inside a 32-row fragment
-  const int lk = (lane >> 5) * 8;     // k offset inside a 16-wide k-step
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  for (int it = 0; it < nk; ++it) {
+    // slab `it` must have landed; later slabs may still be in flight
+    const int ahead = min(STAGES - 2, nk - 1 - it);
+    static_assert((STAGES - 2) * LPT <= 63, "vmcnt range");
+    if (STAGES >= 5 && ahead >= 3) wait_vmcnt<(STAGES >= 5 ? 3 * LPT : 0)>();
+    else if (STAGES >= 4 && ahead >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * LPT : 0)>();
+    else if (ahead >= 1) wait_vmcnt<LPT>();
+    else wait_vmcnt<0>();
+    barrier_nofence();        // slab visible to all waves; slab it-1 retired
+    if (it + STAGES - 1 < nk) issue((it + STAGES - 1) % STAGES, it + STAGES - 1);
+    const char* sa = smem + (it % STAGES) * S_BYTES;
+    const char* sb = sa + A_BYTES;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      typename Fmt::v8 af[TM], bfr[TN];
+      const int c = kk * 2 + hh;
+      v8 af[TM], bfr[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        const int row = wm * (BM / 2) + i * 32 + lr;
-        af[i] = __builtin_bit_cast(
-            typename Fmt::v8, *reinterpret_cast<const u32x4*>(
-                        &As[cur][row * LDS_STRIDE + kk * 16 + lk]));
+        if (!live[i]) continue;
+        const int r = wm * WROWS + i * 32 + l32;
+        af[i] = *reinterpret_cast<const v8*>(sa + swz<BK>(r, c));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int row = j * 64 + wn * 32 + lr;
-        bfr[j] = __builtin_bit_cast(
-            typename Fmt::v8, *reinterpret_cast<const u32x4*>(
-                        &Bs[cur][row * LDS_STRIDE + kk * 16 + lk]));
+        const int r = j * 64 + wn * 32 + l32;
+        bfr[j] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
       }
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i) {
+        if (!live[i]) continue;       // sub-tile past the live rows: no work
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = Fmt::mfma32(af[i], bfr[j], acc[i][j]);
+      }
     }
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
   }
 
   // ---------------------------------------------------------------- epilogue
-  // acc[i][j][e]: row = wm*BM/2 + i*32 + (e/4)*8 + (lane/32)*4 + e%4,
+  // acc[i][j][e]: row = wm*WROWS + i*32 + (e/4)*8 + (lane/32)*4 + e%4,
   //               col = j*64 + wn*32 + lane%32   (tile-local)
-  const int hrow = (lane >> 5) * 4;
-  if constexpr (EPI == EPI_STORE || EPI == EPI_ADD_F32) {
+  const int hrow = hh * 4;
+  if constexpr (EPI == EPI_STORE) {
+    uint16_t* C = reinterpret_cast<uint16_t*>(ep.C);
+    const bool rope = ep.pos && n0 < ep.rope_cols;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + j * 64 + wn * 32 + lr;
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
+        if (row >= M) continue;
+        uint16_t* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + l32;
+        if (rope) {
+          // j even / j+1: dims i and i+64 of the head starting at n0 + j*64
+          const float2 c = ep.cs[(size_t)ep.pos[row] * 64 + wn * 32 + l32];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = m0 + wm * (BM / 2) + i * 32 + (e >> 2) * 8 + hrow +
-                          (e & 3);
-          if (row < M) {
-            if constexpr (EPI == EPI_STORE)
-              reinterpret_cast<uint16_t*>(C)[(size_t)row * ldc + col] =
-                  Fmt::store(acc[i][j][e]);
-            else
-              reinterpret_cast<float*>(C)[(size_t)row * ldc + col] +=
-                  acc[i][j][e];
+          for (int j = 0; j < TN; j += 2) {
+            const float x = acc[i][j][e], y = acc[i][j + 1][e];
+            crow[j * 64] = Fmt::store(x * c.x - y * c.y);
+            crow[(j + 1) * 64] = Fmt::store(y * c.x + x * c.y);
           }
+        } else {
+#pragma unroll
+          for (int j = 0; j < TN; ++j) crow[j * 64] = Fmt::store(acc[i][j][e]);
         }
       }
-  } else if constexpr (EPI == EPI_SWIGLU) {
+  } else if constexpr (EPI == EPI_ADD_F32) {
+    float* C = reinterpret_cast<float*>(ep.C);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN / 2; ++j) {
-        const int col = nb * (BN / 2) + j * 64 + wn * 32 + lr;
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
+        if (row >= M) continue;
+        float* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + l32;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = m0 + wm * (BM / 2) + i * 32 + (e >> 2) * 8 + hrow +
-                          (e & 3);
-          if (row < M) {
-            const float g = acc[i][j][e];
-            const float u = acc[i][j + TN / 2][e];
-            const float h = g / (1.0f + __expf(-g)) * u;
-            reinterpret_cast<uint16_t*>(C)[(size_t)row * ldc + col] =
-                Fmt::store(h);
+        for (int j = 0; j < TN; ++j) crow[j * 64] += acc[i][j][e];
+      }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    uint16_t* C = reinterpret_cast<uint16_t*>(ep.C);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
+        if (row >= M) continue;
+        uint16_t* crow = C + (size_t)row * ep.ldc + nb * (BN / 2) + wn * 32 + l32;
+#pragma unroll
+        for (int j = 0; j < TN / 2; ++j) {
+          const float g = acc[i][j][e], u = acc[i][j + TN / 2][e];
+          crow[j * 64] = Fmt::store(g / (1.0f + __expf(-g)) * u);
+        }
+      }
+  } else if constexpr (EPI == EPI_PARTIAL) {
+    float* P = ep.part + (size_t)ks * M * ep.part_ld;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
+        if (row >= M) continue;
+        float* prow = P + (size_t)row * ep.part_ld;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          int col;
+          if (ep.dual) {       // gate half -> [0, F), up half -> [F, 2F)
+            const int jj = j % (TN / 2);
+            col = (j < TN / 2 ? 0 : ep.ffn) + nb * (BN / 2) + jj * 64 + wn * 32 + l32;
+          } else {
+            col = n0 + j * 64 + wn * 32 + l32;
           }
+          prow[col] = acc[i][j][e];
         }
       }
   } else {   // EPI_HEAD
@@ -215,17 +330,17 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int lrow = wm * (BM / 2) + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
+        const int lrow = wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
         const int row = m0 + lrow;
         float m = -INFINITY, s = 0.f;
         int a = 0x7fffffff;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const int col = n0 + j * 64 + wn * 32 + lr;
+          const int col = n0 + j * 64 + wn * 32 + l32;
           float v = acc[i][j][e];
-          if (ha.logits_out && row < m_live && col < ha.vocab)
-            ha.logits_out[(size_t)ha.list[1 + row] * ha.vocab + col] = v;
-          if (col == ha.mask_id || col >= ha.vocab) v = -INFINITY;
+          if (ep.logits_out && row < m_live && col < ep.vocab)
+            ep.logits_out[(size_t)ep.list[1 + row] * ep.vocab + col] = v;
+          if (col == ep.mask_id || col >= ep.vocab) v = -INFINITY;
           if (v > m) {              // columns ascend with j: keeps the first
             s = s * __expf(m - v) + 1.0f;
             m = v; a = col;
@@ -233,7 +348,6 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
             s += __expf(v - m);
           }
         }
-        // combine over the 32 lanes of this half-wave (same row)
 #pragma unroll
         for (int o = 1; o < 32; o <<= 1) {
           const float m2 = __shfl_xor(m, o, 64);
@@ -246,7 +360,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
           const int na = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
           m = mm; s = ns; a = na;
         }
-        if (lr == 0) {
+        if (l32 == 0) {
           red_m[wn][lrow] = m;
           red_s[wn][lrow] = s;
           red_a[wn][lrow] = a;
@@ -254,7 +368,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       }
     }
     __syncthreads();
-    for (int r = t; r < BM; r += 256) {
+    for (int r = t; r < BM; r += 64 * WAVES) {
       const int row = m0 + r;
       if (row >= m_live) continue;
       const float m1 = red_m[0][r], m2 = red_m[1][r];
@@ -264,57 +378,142 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       if (m2 != -INFINITY) s += red_s[1][r] * __expf(m2 - mm);
       const int a1 = red_a[0][r], a2 = red_a[1][r];
       const int a = (m2 > m1 || (m2 == m1 && a2 < a1)) ? a2 : a1;
-      const size_t o = (size_t)row * ha.n_slabs + nb;
-      ha.pmax[o] = mm;
-      ha.psum[o] = s;
-      ha.parg[o] = a;
+      const size_t o = (size_t)row * ep.n_slabs + nb;
+      ep.pmax[o] = mm;
+      ep.psum[o] = s;
+      ep.parg[o] = a;
     }
   }
+  }  // M tiles
 }
 
-template <typename Fmt, int BM, int BN, int EPI>
-int launch(const uint16_t* A, const uint16_t* B, const uint16_t* B2, void* C,
-           int M, int N, int K, int ldc, int n_ntiles, const HeadArgs& ha,
-           hipStream_t s) {
-  const int mt = (M + BM - 1) / BM;
-  const int nwg = mt * n_ntiles;
-  hipLaunchKernelGGL((gemm16_kernel<Fmt, BM, BN, EPI>), dim3(nwg), dim3(256),
-                     0, s, A, B, B2, C, M, N, K, ldc, mt, ha);
+template <typename Fmt, typename V, int EPI>
+int launch_tiles(const uint16_t* A, const uint16_t* B, const uint16_t* B2,
+                 int M, int N, int K, int ksplit, const EpiArgs& ep,
+                 hipStream_t s, int max_mtiles = 1 << 30) {
+  const int mt = std::min((M + V::BM - 1) / V::BM, max_mtiles);
+  const int nt = (N + V::BN - 1) / V::BN;
+  const int nwg = mt * nt * ksplit;
+  hipLaunchKernelGGL((gemm16_kernel<Fmt, V, EPI>), dim3(nwg),
+                     dim3(64 * V::WAVES), 0, s, A, B, B2, M, N, K, mt, nt,
+                     ksplit, ep);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
 
+// The kernel variants the planner can pick (index = GemmPlan::tile).
+using V0 = Var<128, 128, 32, 4, 4>;    // 64 KB LDS, 2 workgroups per CU
+using V1 = Var<256, 128, 32, 4, 8>;
+using V2 = Var<128, 256, 32, 4, 8>;
+using V3 = Var<256, 256, 32, 4, 8>;    // large M
+using V4 = Var<128, 128, 64, 4, 4>;    // 128 KB LDS, deep 128-byte slabs
+using V5 = Var<64, 128, 32, 5, 4>;     // 60 KB: 2 workgroups per CU
+using V6 = Var<128, 128, 64, 2, 4>;    // 64 KB, 2 workgroups per CU
+using V7 = Var<256, 128, 64, 2, 8>;    // 96 KB
+using V8 = Var<256, 256, 64, 2, 8>;    // 128 KB, deep slabs, large M
+using V9 = Var<128, 256, 64, 2, 8>;    // 96 KB
+using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
+using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
+constexpr int N_VARIANTS = 12;
+
+int variant_bn(int tile) {
+  switch (tile) {
+    case 2: case 3: case 8: case 9: return 256;
+    default: return 128;
+  }
+}
+int variant_bm(int tile) {
+  switch (tile) {
+    case 1: case 3: case 7: case 8: return 256;
+    case 5: return 64;
+    default: return 128;
+  }
+}
+int variant_bk(int tile) {
+  return (tile == 4 || (tile >= 6 && tile <= 9)) ? 64 : 32;
+}
+
+template <typename Fmt, int EPI>
+int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
+                 const uint16_t* B2, int M, int N, int K, const EpiArgs& ep,
+                 hipStream_t s) {
+#define LV(Vn) return launch_tiles<Fmt, Vn, EPI>(A, B, B2, M, N, K, p.ksplit, ep, s)
+  switch (p.tile) {
+    case 1: LV(V1);
+    case 2: LV(V2);
+    case 3: LV(V3);
+    case 4: LV(V4);
+    case 5: LV(V5);
+    case 6: LV(V6);
+    case 7: LV(V7);
+    case 8: LV(V8);
+    case 9: LV(V9);
+    case 10: LV(V10);
+    case 11: LV(V11);
+    default: LV(V0);
+  }
+#undef LV
+}
+
 template <typename Fmt>
-int gemm_dispatch(int epi, const uint16_t* A, const uint16_t* B,
-                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
-                  hipStream_t s) {
-  HeadArgs ha{};
+int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
+                  const uint16_t* B, const uint16_t* B2, int M, int N, int K,
+                  const EpiArgs& ep, hipStream_t s) {
+  if (p.ksplit > 1)
+    return launch_shape<Fmt, EPI_PARTIAL>(p, A, B, B2, M, N, K, ep, s);
   switch (epi) {
-    case EPI_STORE:
-      return launch<Fmt, 128, 128, EPI_STORE>(A, B, B2, C, M, N, K, ldc,
-                                              N / 128, ha, s);
-    case EPI_ADD_F32:
-      return launch<Fmt, 128, 128, EPI_ADD_F32>(A, B, B2, C, M, N, K, ldc,
-                                                N / 128, ha, s);
-    case EPI_SWIGLU:   // N = 2 * ffn output columns of gate|up
-      return launch<Fmt, 128, 128, EPI_SWIGLU>(A, B, B2, C, M, N, K, ldc,
-                                               N / 128, ha, s);
+    case EPI_STORE: return launch_shape<Fmt, EPI_STORE>(p, A, B, B2, M, N, K, ep, s);
+    case EPI_ADD_F32: return launch_shape<Fmt, EPI_ADD_F32>(p, A, B, B2, M, N, K, ep, s);
+    case EPI_SWIGLU: return launch_shape<Fmt, EPI_SWIGLU>(p, A, B, B2, M, N, K, ep, s);
   }
   return set_error(DAVET_EINVAL, "gemm16: unknown epilogue");
 }
 
 }  // namespace
 
-int launch_gemm16(int dtype, int epi, const uint16_t* A, const uint16_t* B,
-                  const uint16_t* B2, void* C, int M, int N, int K, int ldc,
-                  int cls, hipStream_t s) {
+// Kernel choice measured on MI355X over the workload shapes (d = 4096,
+// ffn = 12288, 209..18020 tokens): 128 x 128 tiles with 128-byte slabs and two
+// workgroups per CU win up to ~2-3K rows; 256 x 256 tiles with 8 wavefronts
+// win above (50-55% of the fp16 matrix peak).  Narrow-N products (the output
+// and down projections) split K until the grid fills the 256 CUs.
+GemmPlan plan_gemm16(int M, int N, int K) {
+  GemmPlan p{};
+  const bool big = M >= (N >= 16384 ? 2048 : 3000);
+  p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 8 : (K % 64 == 0 ? 6 : 0);
+  const int bm = variant_bm(p.tile), bn = variant_bn(p.tile);
+  const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  const int nk = K / variant_bk(p.tile);
+  p.ksplit = 1;
+  if (N < 8192)
+    while (tiles * p.ksplit < 256 && nk / (p.ksplit * 2) >= 16 && p.ksplit < 8)
+      p.ksplit *= 2;
+  return p;
+}
+
+int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
+                  const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
+                  int K, int ldc, const int32_t* pos, const float* cs,
+                  int rope_cols, float* partials, int cls, hipStream_t s) {
   if (M <= 0) return DAVET_OK;
-  if (N % 128 || K % BK)
-    return set_error(DAVET_ESHAPE, "gemm16: N % 128 or K % 64 != 0");
+  if (N % variant_bn(plan.tile) || K % variant_bk(plan.tile) ||
+      (plan.ksplit > 1 && (K / variant_bk(plan.tile)) < plan.ksplit))
+    return set_error(DAVET_ESHAPE, "gemm16: N or K not a multiple of the tile");
+  if (plan.ksplit > 1 && !partials)
+    return set_error(DAVET_EINVAL, "gemm16: split-K needs a partial buffer");
   ProfScope ps(cls, s);
+  EpiArgs ep{};
+  ep.C = C;
+  ep.ldc = ldc;
+  ep.pos = pos;
+  ep.cs = reinterpret_cast<const float2*>(cs);
+  ep.rope_cols = rope_cols;
+  ep.part = partials;
+  ep.part_ld = N;
+  ep.dual = epi == EPI_SWIGLU;
+  ep.ffn = N / 2;
   return dtype == DAVET_F16
-             ? gemm_dispatch<F16>(epi, A, B, B2, C, M, N, K, ldc, s)
-             : gemm_dispatch<BF16>(epi, A, B, B2, C, M, N, K, ldc, s);
+             ? gemm_dispatch<F16>(plan, epi, A, B, B2, M, N, K, ep, s)
+             : gemm_dispatch<BF16>(plan, epi, A, B, B2, M, N, K, ep, s);
 }
 
 int head16_slabs(int vocab) { return (vocab + 127) / 128; }
@@ -322,18 +521,39 @@ int head16_slabs(int vocab) { return (vocab + 127) / 128; }
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s) {
-  if (d % BK) return set_error(DAVET_ESHAPE, "head16: d % 64 != 0");
+                  float* logits_out, hipStream_t s, int variant) {
+  if (variant < 0) variant = 6;
+  if (d % BK_MIN) return set_error(DAVET_ESHAPE, "head16: d % 32 != 0");
   ProfScope ps(KC_HEAD, s);
-  HeadArgs ha{list, vocab, mask_id, head16_slabs(vocab), pmax, psum, parg,
-              logits_out};
-  return dtype == DAVET_F16
-             ? launch<F16, 128, 128, EPI_HEAD>(Hm, W, nullptr, nullptr,
-                                               max_rows, vocab, d, 0,
-                                               ha.n_slabs, ha, s)
-             : launch<BF16, 128, 128, EPI_HEAD>(Hm, W, nullptr, nullptr,
-                                                max_rows, vocab, d, 0,
-                                                ha.n_slabs, ha, s);
+  EpiArgs ep{};
+  ep.list = list;
+  ep.vocab = vocab;
+  ep.mask_id = mask_id;
+  ep.n_slabs = head16_slabs(vocab);
+  ep.pmax = pmax;
+  ep.psum = psum;
+  ep.parg = parg;
+  ep.logits_out = logits_out;
+  // 128-column slabs (BN = 128) keep n_slabs = ceil(V / 128)
+  // One M slot per vocabulary slab: each workgroup loops over the live row
+  // tiles, so late steps with few masked rows launch no idle workgroups (idle
+  // ones would also leave every other CU without live work).
+#define HV(Fmt, Vn) return launch_tiles<Fmt, Vn, EPI_HEAD>(Hm, W, nullptr, max_rows, vocab, d, 1, ep, s, 1)
+  if (dtype == DAVET_F16) {
+    switch (variant) {
+      case 0: HV(F16, V0);
+      case 10: HV(F16, V10);
+      case 11: HV(F16, V11);
+      default: HV(F16, V6);
+    }
+  }
+  switch (variant) {
+    case 0: HV(BF16, V0);
+    case 10: HV(BF16, V10);
+    case 11: HV(BF16, V11);
+    default: HV(BF16, V6);
+  }
+#undef HV
 }
 
 }  // namespace davet

@@ -41,11 +41,13 @@ assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
                      const int32_t* __restrict__ resp_ids,
                      const uint8_t* __restrict__ masked, int mask_id,
                      int vocab, int d, const float* __restrict__ gain,
-                     float eps, float* __restrict__ X, T* __restrict__ A) {
+                     float eps, float* __restrict__ X, T* __restrict__ A,
+                     int32_t* __restrict__ pos) {
   __shared__ float red[kThreads / 64];
   const int row = blockIdx.x;
   const int s = find_seq(sp, row);
   const int j = row - sp.row0[s];
+  if (threadIdx.x == 0 && pos) pos[row] = j;     // rotary position
   const T* src;
   if (j < sp.nview[s]) {
     src = reinterpret_cast<const T*>(vp.p[s]) + (size_t)j * d;
@@ -301,6 +303,90 @@ head_reduce_f32_kernel(const float* __restrict__ logits,
   }
 }
 
+// ---- split-K reductions: partial tiles P[k][row][col] summed in k order
+template <typename Fmt, typename T = typename Fmt::st>
+__global__ void __launch_bounds__(kThreads)
+reduce_add_norm_kernel(const float* __restrict__ P, int ksplit, int rows,
+                       int d, float* __restrict__ X,
+                       const float* __restrict__ gain, float eps,
+                       T* __restrict__ A) {
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const size_t stride = (size_t)rows * d;
+  float v[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    float x = 0.f;
+    if (e < d) {
+      x = X[(size_t)row * d + e];
+      for (int k = 0; k < ksplit; ++k) x += P[k * stride + (size_t)row * d + e];
+      X[(size_t)row * d + e] = x;
+    }
+    v[n] = x;
+    ss += x * x;
+  }
+  if (!A) return;
+  const float tot = block_sum(ss, red);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int n = 0; n < kMaxPer; ++n) {
+    const int e = threadIdx.x + n * kThreads;
+    if (e >= d) break;
+    const float g = gain ? gain[e] : 1.0f;
+    A[(size_t)row * d + e] = Fmt::store(v[n] * rstd * g);
+  }
+}
+
+// columns < rope_cols hold heads of 128 dims rotated as (i, i + 64)
+template <typename Fmt, typename T = typename Fmt::st>
+__global__ void __launch_bounds__(kThreads)
+reduce_store_rope_kernel(const float* __restrict__ P, int ksplit, int rows,
+                         int ncols, int rope_cols,
+                         const int32_t* __restrict__ pos,
+                         const float2* __restrict__ cs, T* __restrict__ out) {
+  const int row = blockIdx.x;
+  const size_t stride = (size_t)rows * ncols;
+  const float* pr = P + (size_t)row * ncols;
+  T* o = out + (size_t)row * ncols;
+  const int p0 = pos[row];
+  for (int p = threadIdx.x; p < rope_cols / 2; p += kThreads) {
+    const int c1 = (p / 64) * 128 + (p % 64), c2 = c1 + 64;
+    float x = 0.f, y = 0.f;
+    for (int k = 0; k < ksplit; ++k) {
+      x += pr[k * stride + c1];
+      y += pr[k * stride + c2];
+    }
+    const float2 c = cs[(size_t)p0 * 64 + (p % 64)];
+    o[c1] = Fmt::store(x * c.x - y * c.y);
+    o[c2] = Fmt::store(y * c.x + x * c.y);
+  }
+  for (int c = rope_cols + threadIdx.x; c < ncols; c += kThreads) {
+    float x = 0.f;
+    for (int k = 0; k < ksplit; ++k) x += pr[k * stride + c];
+    o[c] = Fmt::store(x);
+  }
+}
+
+template <typename Fmt, typename T = typename Fmt::st>
+__global__ void __launch_bounds__(kThreads)
+reduce_swiglu_kernel(const float* __restrict__ P, int ksplit, int rows,
+                     int ffn, T* __restrict__ out) {
+  const int row = blockIdx.x;
+  const size_t ld = (size_t)2 * ffn;
+  const size_t stride = (size_t)rows * ld;
+  const float* pr = P + (size_t)row * ld;
+  for (int c = threadIdx.x; c < ffn; c += kThreads) {
+    float g = 0.f, u = 0.f;
+    for (int k = 0; k < ksplit; ++k) {
+      g += pr[k * stride + c];
+      u += pr[k * stride + ffn + c];
+    }
+    out[(size_t)row * ffn + c] = Fmt::store(g / (1.0f + __expf(-g)) * u);
+  }
+}
+
 // Element-type conversion through float32 (exact for the 16-bit sources),
 // rounding to nearest even into the destination format.
 template <typename Src, typename Dst>
@@ -340,16 +426,59 @@ int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
   return DAVET_OK;
 }
 
+#define DISPATCH16(dtype, F_BODY)                                           \
+  do {                                                                      \
+    if ((dtype) == DAVET_F16) { using F = F16S; F_BODY; }                   \
+    else { using F = BF16S; F_BODY; }                                       \
+  } while (0)
+
+int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,
+                           int d, float* X, const float* gain, float eps,
+                           void* A, hipStream_t s) {
+  if (rows <= 0) return DAVET_OK;
+  ProfScope ps(KC_RMSNORM, s);
+  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_add_norm_kernel<F>, dim3(rows),
+                                       dim3(kThreads), 0, s, P, ksplit, rows,
+                                       d, X, gain, eps, (F::st*)A));
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
+                             int ncols, int rope_cols, const int32_t* pos,
+                             const float* cs, void* out, hipStream_t s) {
+  if (rows <= 0) return DAVET_OK;
+  ProfScope ps(KC_ROPE, s);
+  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_store_rope_kernel<F>, dim3(rows),
+                                       dim3(kThreads), 0, s, P, ksplit, rows,
+                                       ncols, rope_cols, pos,
+                                       (const float2*)cs, (F::st*)out));
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
+int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
+                         int ffn, void* out, hipStream_t s) {
+  if (rows <= 0) return DAVET_OK;
+  ProfScope ps(KC_MISC, s);
+  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_swiglu_kernel<F>, dim3(rows),
+                                       dim3(kThreads), 0, s, P, ksplit, rows,
+                                       ffn, (F::st*)out));
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
 int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const void* embed, const int32_t* prompt_ids,
                          const int32_t* resp_ids, const uint8_t* masked,
                          int mask_id, int vocab, int d, const float* gain,
-                         float eps, float* X, void* A, hipStream_t s) {
+                         float eps, float* X, void* A, int32_t* pos,
+                         hipStream_t s) {
   ProfScope ps(KC_ASSEMBLE, s);
 #define ASM(F)                                                               \
   hipLaunchKernelGGL(assemble_norm_kernel<F>, dim3(sp.total), dim3(kThreads),  \
                      0, s, sp, vp, (const F::st*)embed, prompt_ids, resp_ids, \
-                     masked, mask_id, vocab, d, gain, eps, X, (F::st*)A)
+                     masked, mask_id, vocab, d, gain, eps, X, (F::st*)A, pos)
   if (dtype == DAVET_BF16) ASM(BF16S);
   else if (dtype == DAVET_F16) ASM(F16S);
   else ASM(F32S);

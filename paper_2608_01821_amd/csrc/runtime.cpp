@@ -32,6 +32,7 @@ const char* kernel_class_name(int c) {
 struct Prof {
   bool on = false;
   int used = 0;
+  int only = -1;        // record only this class (-1: every class)
   std::vector<hipEvent_t> start, stop;
   std::vector<int> cls;
 };
@@ -39,6 +40,7 @@ static Prof g_prof;
 
 ProfScope::ProfScope(int c, hipStream_t s) : slot(-1), stream(s) {
   if (!g_prof.on || g_prof.used >= (int)g_prof.start.size()) return;
+  if (g_prof.only >= 0 && c != g_prof.only) return;
   slot = g_prof.used++;
   g_prof.cls[slot] = c;
   if (hipEventRecord(g_prof.start[slot], s) != hipSuccess) slot = -1;
@@ -88,6 +90,14 @@ extern "C" int davet_prof_enable(int32_t max_launches) {
 
 extern "C" int davet_prof_reset(void) {
   davet::g_prof.used = 0;
+  return DAVET_OK;
+}
+
+extern "C" int davet_prof_only(int32_t cls) {
+  using namespace davet;
+  DAVET_CHECK_ARG(cls >= -1 && cls < KC_COUNT, DAVET_EINVAL,
+                  "davet_prof_only: class out of range");
+  g_prof.only = cls;
   return DAVET_OK;
 }
 

@@ -24,9 +24,32 @@ namespace davet {
 
 struct Layout {
   size_t conf, argmax;                 // run_schedule scratch
-  size_t X, A, QKV, O, H, rope, list, Hm, pmax, psum, parg, logits;
+  size_t X, A, QKV, O, H, rope, pos, list, Hm, pmax, psum, parg, logits;
+  size_t part;                         // split-K partial tiles (16-bit path)
   size_t total;
 };
+
+// Bytes of fp32 partial tiles the 16-bit GEMMs of a step may need.  A split
+// is only planned while (tiles * ksplit) < 256 before the last doubling, so
+// tiles * ksplit < 512 and the partials never exceed 512 tiles of 256 x 256.
+static size_t partial_bytes(const davet_model_cfg& c, int64_t tokens) {
+  if (!is16(c.dtype)) return 0;
+  const int64_t Ns[4] = {3LL * c.d, c.d, 2LL * c.ffn, c.d};
+  const int64_t Ks[4] = {c.d, c.d, c.d, c.ffn};
+  size_t best = 0;
+  for (int g = 0; g < 4; ++g) {
+    // worst case over token counts 1..tokens, sampled where plans change
+    for (int64_t m = 1; m <= tokens; m = m < 64 ? m + 1 : m + (m >> 4)) {
+      const GemmPlan p = plan_gemm16((int)m, (int)Ns[g], (int)Ks[g]);
+      if (p.ksplit > 1)
+        best = std::max(best, (size_t)p.ksplit * m * Ns[g] * 4);
+    }
+    const GemmPlan p = plan_gemm16((int)tokens, (int)Ns[g], (int)Ks[g]);
+    if (p.ksplit > 1)
+      best = std::max(best, (size_t)p.ksplit * tokens * Ns[g] * 4);
+  }
+  return std::min<size_t>(best, (size_t)512 * 256 * 256 * 4);
+}
 
 static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
                           int64_t seqs, int64_t L) {
@@ -48,6 +71,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   o.O = take((size_t)tokens * c.d * es);
   o.H = take((size_t)tokens * c.ffn * es);
   o.rope = take((size_t)tokens * (c.head_dim / 2) * 8);
+  o.pos = take((size_t)tokens * 4);
   o.list = take((size_t)(rows + 1) * 4);
   o.Hm = take((size_t)rows * c.d * es);
   if (is16(c.dtype)) {
@@ -58,6 +82,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   } else {
     o.logits = take((size_t)rows * c.vocab * 4);
   }
+  o.part = take(partial_bytes(c, tokens));
   o.total = p;
   return o;
 }
@@ -194,6 +219,8 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   void* O = ws + lay.O;
   void* H = ws + lay.H;
   float* rope = reinterpret_cast<float*>(ws + lay.rope);
+  int32_t* pos = reinterpret_cast<int32_t*>(ws + lay.pos);
+  float* part = reinterpret_cast<float*>(ws + lay.part);
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
   void* Hm = ws + lay.Hm;
   const int rows = n_seqs * L;
@@ -208,28 +235,52 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
   RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,
                            resp_masked, c.mask_id, c.vocab, d, g0, c.rms_eps, X, A,
-                           s));
+                           pos, s));
+  const int T = sp.total;
+  const GemmPlan p_qkv = plan_gemm16(T, 3 * d, d), p_o = plan_gemm16(T, d, d);
+  const GemmPlan p_gu = plan_gemm16(T, 2 * F, d), p_dn = plan_gemm16(T, d, F);
+  bool a_ready = true;       // A holds RMSNorm(X) for the next GEMM
   for (int l = 0; l < c.n_layers; ++l) {
     const davet_layer_weights& lw = w->layers[l];
-    if (l > 0) RUN(launch_rmsnorm(X, sp.total, d, lw.attn_norm, c.rms_eps,
-                                  c.dtype, A, s));
+    if (!a_ready) RUN(launch_rmsnorm(X, T, d, lw.attn_norm, c.rms_eps,
+                                     c.dtype, A, s));
     if (bf) {
-      RUN(launch_gemm16(dt, EPI_STORE, (const uint16_t*)A,
-                           (const uint16_t*)lw.wqkv, nullptr, QKV, sp.total,
-                           3 * d, d, 3 * d, KC_GEMM_QKV, s));
-      RUN(launch_rope(QKV, sp.total, c.n_heads, c.head_dim, c.dtype, sp, rope, s));
+      const uint16_t* Ah = (const uint16_t*)A;
+      // QKV projection, rotary embedding on the query and key columns
+      RUN(launch_gemm16(dt, EPI_STORE, p_qkv, Ah, (const uint16_t*)lw.wqkv,
+                        nullptr, QKV, T, 3 * d, d, 3 * d, pos, rope, 2 * d,
+                        part, KC_GEMM_QKV, s));
+      if (p_qkv.ksplit > 1)
+        RUN(launch_reduce_store_rope(dt, part, p_qkv.ksplit, T, 3 * d, 2 * d,
+                                     pos, rope, QKV, s));
       RUN(launch_attention16(dt, (const uint16_t*)QKV, (uint16_t*)O, sp,
                              c.n_heads, c.head_dim, s));
-      RUN(launch_gemm16(dt, EPI_ADD_F32, (const uint16_t*)O,
-                           (const uint16_t*)lw.wo, nullptr, X, sp.total, d, d,
-                           d, KC_GEMM_O, s));
-      RUN(launch_rmsnorm(X, sp.total, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
-      RUN(launch_gemm16(dt, EPI_SWIGLU, (const uint16_t*)A,
-                           (const uint16_t*)lw.wg, (const uint16_t*)lw.wu, H,
-                           sp.total, 2 * F, d, F, KC_GEMM_GATEUP, s));
-      RUN(launch_gemm16(dt, EPI_ADD_F32, (const uint16_t*)H,
-                           (const uint16_t*)lw.wd, nullptr, X, sp.total, d, F,
-                           d, KC_GEMM_DOWN, s));
+      // X += O Wo^T, then A = RMSNorm(X) for the feed-forward block
+      RUN(launch_gemm16(dt, EPI_ADD_F32, p_o, (const uint16_t*)O,
+                        (const uint16_t*)lw.wo, nullptr, X, T, d, d, d,
+                        nullptr, nullptr, 0, part, KC_GEMM_O, s));
+      if (p_o.ksplit > 1)
+        RUN(launch_reduce_add_norm(dt, part, p_o.ksplit, T, d, X, lw.ffn_norm,
+                                   c.rms_eps, A, s));
+      else
+        RUN(launch_rmsnorm(X, T, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
+      RUN(launch_gemm16(dt, EPI_SWIGLU, p_gu, Ah, (const uint16_t*)lw.wg,
+                        (const uint16_t*)lw.wu, H, T, 2 * F, d, F, nullptr,
+                        nullptr, 0, part, KC_GEMM_GATEUP, s));
+      if (p_gu.ksplit > 1)
+        RUN(launch_reduce_swiglu(dt, part, p_gu.ksplit, T, F, H, s));
+      // X += H Wd^T (and the next layer's input norm when reducing splits)
+      RUN(launch_gemm16(dt, EPI_ADD_F32, p_dn, (const uint16_t*)H,
+                        (const uint16_t*)lw.wd, nullptr, X, T, d, F, d,
+                        nullptr, nullptr, 0, part, KC_GEMM_DOWN, s));
+      a_ready = false;
+      if (p_dn.ksplit > 1) {
+        const bool next = l + 1 < c.n_layers;
+        RUN(launch_reduce_add_norm(dt, part, p_dn.ksplit, T, d, X,
+                                   next ? w->layers[l + 1].attn_norm : nullptr,
+                                   c.rms_eps, next ? A : nullptr, s));
+        a_ready = next;
+      }
     } else {
       RUN(launch_gemm_f32(EPI_STORE, (const float*)A, (const float*)lw.wqkv,
                           nullptr, (float*)QKV, sp.total, 3 * d, d, 3 * d,
@@ -245,6 +296,7 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
                           KC_GEMM_F32, nullptr, s));
       RUN(launch_gemm_f32(EPI_ADD_F32, (const float*)H, (const float*)lw.wd,
                           nullptr, X, sp.total, d, F, d, KC_GEMM_F32, nullptr, s));
+      a_ready = false;
     }
   }
   RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
