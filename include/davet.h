@@ -187,6 +187,8 @@ int davet_workspace_bytes(const davet_model_cfg* cfg, int32_t max_tokens,
  *   argmax_out int32 [n_seqs*L];
  *   logits_out float [n_seqs*L, vocab] or NULL: when given, the logits of
  *   masked positions are stored in their rows (other rows untouched).
+ *   Weight matrices, norm vectors and view rows are read with 16-byte
+ *   vector loads: their pointers must be 16-byte aligned (EINVAL otherwise).
  * Errors: EINVAL, ESHAPE (head_dim, d, ffn, n_seqs, L or token counts out of
  * range), EDTYPE, ENOMEM (ws_bytes too small or workspace misaligned). */
 int davet_denoise_step(const davet_model_cfg* cfg, const davet_weights* w,

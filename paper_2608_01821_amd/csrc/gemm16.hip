@@ -34,6 +34,11 @@ namespace davet {
 namespace {
 
 constexpr int BK_MIN = 32;   // K must be a multiple of this
+
+// K-order rotation of the vocabulary head (see launch_head16)
+#ifndef DAVET_HEAD_KROT
+#define DAVET_HEAD_KROT 0
+#endif
 constexpr int EPI_HEAD = 3;
 
 // Kernel variants: tile BM x BN, K slab BK (64-byte or 128-byte LDS rows),
@@ -67,6 +72,9 @@ struct EpiArgs {
   int part_ld;
   int dual;              // B/B2 gate/up weights (SwiGLU), also for partials
   int ffn;
+  // K order: N tile nb starts at slab (nb * krot) mod nk and wraps, so that
+  // concurrent workgroups stream different DRAM regions (0: in order)
+  int krot;
 };
 
 __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
@@ -79,6 +87,19 @@ __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in [LO, HI] known only at run time
+// (the count is an instruction immediate): a binary tree of scalar branches.
+template <int LO, int HI>
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+  if constexpr (LO == HI) {
+    wait_vmcnt<LO>();
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (n <= MID) wait_vmcnt_rt<LO, MID>(n);
+    else wait_vmcnt_rt<MID + 1, HI>(n);
+  }
 }
 
 // Workgroup barrier without the memory fence __syncthreads() carries: the
@@ -181,12 +202,22 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     b_src[q] = base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
   }
 
+  // A load instructions of this wave holding at least one live row: rows
+  // past the last live one are not fetched (their LDS rows feed only output
+  // rows that are never stored).  The count is wave-uniform, so the per-slab
+  // load count LPT_live of each wave is too.
+  const int na = __builtin_amdgcn_readfirstlane(
+      max(0, min(AI, (m_live - m0 - wave * AI * RPI + RPI - 1) / RPI)));
+  const int lpt_live = na + BI;
+  const int rot = ep.krot ? (int)(((long)nb * ep.krot) % nk) : 0;
   auto issue = [&](int stage, int kt) {
+    kt += rot;
+    if (kt >= nk) kt -= nk;
     char* sa = smem + stage * S_BYTES;
     char* sb = sa + A_BYTES;
 #pragma unroll
     for (int q = 0; q < AI; ++q)
-      dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
+      if (q < na) dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
 #pragma unroll
     for (int q = 0; q < BI; ++q)
       dma16(b_src[q] + (size_t)kt * BK, sb + (wave * BI + q) * 1024);
@@ -213,10 +244,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     // slab `it` must have landed; later slabs may still be in flight
     const int ahead = min(STAGES - 2, nk - 1 - it);
     static_assert((STAGES - 2) * LPT <= 63, "vmcnt range");
-    if (STAGES >= 5 && ahead >= 3) wait_vmcnt<(STAGES >= 5 ? 3 * LPT : 0)>();
-    else if (STAGES >= 4 && ahead >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * LPT : 0)>();
-    else if (ahead >= 1) wait_vmcnt<LPT>();
-    else wait_vmcnt<0>();
+    wait_vmcnt_rt<0, (STAGES - 2) * LPT>(ahead * lpt_live);
     barrier_nofence();        // slab visible to all waves; slab it-1 retired
     if (it + STAGES - 1 < nk) issue((it + STAGES - 1) % STAGES, it + STAGES - 1);
     const char* sa = smem + (it % STAGES) * S_BYTES;
@@ -511,6 +539,7 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
   ep.part_ld = N;
   ep.dual = epi == EPI_SWIGLU;
   ep.ffn = N / 2;
+  ep.krot = plan.krot;
   return dtype == DAVET_F16
              ? gemm_dispatch<F16>(plan, epi, A, B, B2, M, N, K, ep, s)
              : gemm_dispatch<BF16>(plan, epi, A, B, B2, M, N, K, ep, s);
@@ -521,8 +550,12 @@ int head16_slabs(int vocab) { return (vocab + 127) / 128; }
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s, int variant) {
+                  float* logits_out, hipStream_t s, int variant, int krot) {
   if (variant < 0) variant = 6;
+  // K-order rotation per vocabulary slab: helps the weight stream of an
+  // isolated head launch on MI355X but not inside the denoising step (the
+  // measured default there is 0, every slab starting at k = 0)
+  if (krot < 0) krot = DAVET_HEAD_KROT;
   if (d % BK_MIN) return set_error(DAVET_ESHAPE, "head16: d % 32 != 0");
   ProfScope ps(KC_HEAD, s);
   EpiArgs ep{};
@@ -534,6 +567,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   ep.psum = psum;
   ep.parg = parg;
   ep.logits_out = logits_out;
+  ep.krot = krot;
   // 128-column slabs (BN = 128) keep n_slabs = ceil(V / 128)
   // One M slot per vocabulary slab: each workgroup loops over the live row
   // tiles, so late steps with few masked rows launch no idle workgroups (idle

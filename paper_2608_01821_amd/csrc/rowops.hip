@@ -31,7 +31,81 @@ __device__ __forceinline__ int find_seq(const SeqPack& sp, int row) {
   return s;
 }
 
-constexpr int kMaxPer = 32;   // d <= 8192 elements per row
+// Rows are moved in chunks of 8 elements (16 bytes of a 16-bit format, 32 of
+// fp32): d is a multiple of 64, every row start is 16-byte aligned.  A thread
+// owns chunks t, t + 256, ... (at most 4: d <= 8192).
+constexpr int kMaxChunks = 4;
+
+template <typename Fmt>
+__device__ __forceinline__ void load8(const typename Fmt::st* p, float* v) {
+  if constexpr (Fmt::dtype == DAVET_F32) {
+    const float4 a = reinterpret_cast<const float4*>(p)[0];
+    const float4 b = reinterpret_cast<const float4*>(p)[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  } else {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = Fmt::load((uint16_t)(w[i] & 0xffffu));
+      v[2 * i + 1] = Fmt::load((uint16_t)(w[i] >> 16));
+    }
+  }
+}
+
+template <typename Fmt>
+__device__ __forceinline__ void store8(typename Fmt::st* p, const float* v) {
+  if constexpr (Fmt::dtype == DAVET_F32) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+  } else {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)Fmt::store(v[2 * i]) |
+             ((uint32_t)Fmt::store(v[2 * i + 1]) << 16);
+    *reinterpret_cast<u32x4*>(p) = w;
+  }
+}
+
+__device__ __forceinline__ void load8f(const float* p, float* v) {
+  load8<F32S>(p, v);
+}
+__device__ __forceinline__ void store8f(float* p, const float* v) {
+  store8<F32S>(p, v);
+}
+
+// gain chunk (1.0 where no gain vector is given)
+__device__ __forceinline__ void gain8(const float* g, int e, float* v) {
+  if (g) {
+    load8f(g + e, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = 1.0f;
+  }
+}
+
+// A[row] = 16-bit or fp32 RMSNorm of the row chunks x (sum of squares ss of
+// this thread's part).
+template <typename Fmt, typename T = typename Fmt::st>
+__device__ __forceinline__ void norm_store(float (*x)[8], float ss, int d,
+                                           const float* __restrict__ gain,
+                                           float eps, T* __restrict__ out,
+                                           float* red) {
+  const float tot = block_sum(ss, red);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+  const int nc = d / 8;
+#pragma unroll
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c >= nc) break;
+    float g[8], y[8];
+    gain8(gain, c * 8, g);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) y[i] = x[n][i] * rstd * g[i];
+    store8<Fmt>(out + (size_t)c * 8, y);
+  }
+}
 
 // X[row] = [view | E[prompt] | E[resp or mask]] row; A[row] = RMSNorm(X[row]).
 template <typename Fmt, typename T = typename Fmt::st>
@@ -62,24 +136,20 @@ assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
     const int id = masked[q] ? mask_id : min(max(resp_ids[q], 0), vocab - 1);
     src = embed + (size_t)id * d;
   }
-  float x[kMaxPer];
+  const int nc = d / 8;
+  float x[kMaxChunks][8];
   float ss = 0.f;
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    x[n] = e < d ? Fmt::load(src[e]) : 0.f;
-    ss += x[n] * x[n];
-  }
-  const float tot = block_sum(ss, red);
-  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c < nc) {
+      load8<Fmt>(src + (size_t)c * 8, x[n]);
+      store8f(X + (size_t)row * d + c * 8, x[n]);
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    if (e >= d) break;
-    X[(size_t)row * d + e] = x[n];
-    const float g = gain ? gain[e] : 1.0f;
-    A[(size_t)row * d + e] = Fmt::store(x[n] * rstd * g);
+      for (int i = 0; i < 8; ++i) ss += x[n][i] * x[n][i];
+    }
   }
+  norm_store<Fmt>(x, ss, d, gain, eps, A + (size_t)row * d, red);
 }
 
 template <typename Fmt, typename T = typename Fmt::st>
@@ -89,23 +159,19 @@ rmsnorm_kernel(const float* __restrict__ X, int d,
   __shared__ float red[kThreads / 64];
   const int row = blockIdx.x;
   const float* x = X + (size_t)row * d;
-  float v[kMaxPer];
+  const int nc = d / 8;
+  float v[kMaxChunks][8];
   float ss = 0.f;
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    v[n] = e < d ? x[e] : 0.f;
-    ss += v[n] * v[n];
-  }
-  const float tot = block_sum(ss, red);
-  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c < nc) {
+      load8f(x + c * 8, v[n]);
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    if (e >= d) break;
-    const float g = gain ? gain[e] : 1.0f;
-    A[(size_t)row * d + e] = Fmt::store(v[n] * rstd * g);
+      for (int i = 0; i < 8; ++i) ss += v[n][i] * v[n][i];
+    }
   }
+  norm_store<Fmt>(v, ss, d, gain, eps, A + (size_t)row * d, red);
 }
 
 // cos/sin of pos * theta^(-2i/D), evaluated in float64 and rounded once.
@@ -147,30 +213,35 @@ rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
 
 // Single workgroup: ordered list of masked response positions (global index
 // s*L + i) with the count in list[0]; committed positions get conf = -inf and
-// argmax = -1.
+// argmax = -1.  Each thread takes a contiguous run of positions; the run
+// offsets come from a workgroup prefix sum (wavefront scan + LDS).
 __global__ void __launch_bounds__(kThreads)
 head_prep_kernel(int total, const uint8_t* __restrict__ masked,
                  int32_t* __restrict__ list, float* __restrict__ conf_out,
                  int32_t* __restrict__ argmax_out) {
-  __shared__ int part[kThreads];
+  __shared__ int wsum[kThreads / 64];
   const int per = (total + kThreads - 1) / kThreads;
-  const int lo = threadIdx.x * per;
+  const int lo = min(total, (int)threadIdx.x * per);
   const int hi = min(total, lo + per);
   int c = 0;
   for (int i = lo; i < hi; ++i) c += masked[i] != 0;
-  part[threadIdx.x] = c;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int t = 0; t < kThreads; ++t) {
-      const int v = part[t];
-      part[t] = run;
-      run += v;
-    }
-    list[0] = run;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
   }
+  if (lane == 63) wsum[w] = incl;
   __syncthreads();
-  int o = part[threadIdx.x];
+  int base = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) {
+    if (i < w) base += wsum[i];
+    all += wsum[i];
+  }
+  if (threadIdx.x == 0) list[0] = all;
+  int o = base + incl - c;
   for (int i = lo; i < hi; ++i) {
     if (masked[i]) {
       list[1 + o++] = i;
@@ -195,23 +266,19 @@ final_norm_gather_kernel(const float* __restrict__ X, SeqPack sp,
   const int s = g / sp.L, i = g % sp.L;
   const int row = sp.row0[s] + sp.nview[s] + sp.plen[s] + i;
   const float* x = X + (size_t)row * d;
-  float v[kMaxPer];
+  const int nc = d / 8;
+  float v[kMaxChunks][8];
   float ss = 0.f;
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    v[n] = e < d ? x[e] : 0.f;
-    ss += v[n] * v[n];
-  }
-  const float tot = block_sum(ss, red);
-  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c < nc) {
+      load8f(x + c * 8, v[n]);
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    if (e >= d) break;
-    const float gg = gain ? gain[e] : 1.0f;
-    Hm[(size_t)j * d + e] = Fmt::store(v[n] * rstd * gg);
+      for (int q = 0; q < 8; ++q) ss += v[n][q] * v[n][q];
+    }
   }
+  norm_store<Fmt>(v, ss, d, gain, eps, Hm + (size_t)j * d, red);
 }
 
 // (max, first argmax, sum of exp(l - max)) partials over vocabulary slabs ->
@@ -304,86 +371,106 @@ head_reduce_f32_kernel(const float* __restrict__ logits,
 }
 
 // ---- split-K reductions: partial tiles P[k][row][col] summed in k order
-template <typename Fmt, typename T = typename Fmt::st>
+// (fixed order: deterministic), 8-column chunks, every load of a chunk issued
+// before the first add.
+template <int KS>
+__device__ __forceinline__ void sum_parts(const float* __restrict__ p,
+                                          size_t stride, float* v) {
+  float t[KS][8];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) load8f(p + k * stride, t[k]);
+#pragma unroll
+  for (int k = 0; k < KS; ++k)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[k][i];
+}
+
+// X[row] += sum_k P[k][row]; then A[row] = RMSNorm(X[row]) * gain if A given.
+template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
-reduce_add_norm_kernel(const float* __restrict__ P, int ksplit, int rows,
-                       int d, float* __restrict__ X,
-                       const float* __restrict__ gain, float eps,
-                       T* __restrict__ A) {
+reduce_add_norm_kernel(const float* __restrict__ P, int rows, int d,
+                       float* __restrict__ X, const float* __restrict__ gain,
+                       float eps, T* __restrict__ A) {
   __shared__ float red[kThreads / 64];
   const int row = blockIdx.x;
   const size_t stride = (size_t)rows * d;
-  float v[kMaxPer];
+  const int nc = d / 8;
+  float v[kMaxChunks][8];
   float ss = 0.f;
 #pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    float x = 0.f;
-    if (e < d) {
-      x = X[(size_t)row * d + e];
-      for (int k = 0; k < ksplit; ++k) x += P[k * stride + (size_t)row * d + e];
-      X[(size_t)row * d + e] = x;
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c < nc) {
+      float* xr = X + (size_t)row * d + c * 8;
+      load8f(xr, v[n]);
+      sum_parts<KS>(P + (size_t)row * d + c * 8, stride, v[n]);
+      store8f(xr, v[n]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss += v[n][i] * v[n][i];
     }
-    v[n] = x;
-    ss += x * x;
   }
   if (!A) return;
-  const float tot = block_sum(ss, red);
-  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
-#pragma unroll
-  for (int n = 0; n < kMaxPer; ++n) {
-    const int e = threadIdx.x + n * kThreads;
-    if (e >= d) break;
-    const float g = gain ? gain[e] : 1.0f;
-    A[(size_t)row * d + e] = Fmt::store(v[n] * rstd * g);
-  }
+  norm_store<Fmt>(v, ss, d, gain, eps, A + (size_t)row * d, red);
 }
 
 // columns < rope_cols hold heads of 128 dims rotated as (i, i + 64)
-template <typename Fmt, typename T = typename Fmt::st>
+template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
-reduce_store_rope_kernel(const float* __restrict__ P, int ksplit, int rows,
-                         int ncols, int rope_cols,
-                         const int32_t* __restrict__ pos,
+reduce_store_rope_kernel(const float* __restrict__ P, int rows, int ncols,
+                         int rope_cols, const int32_t* __restrict__ pos,
                          const float2* __restrict__ cs, T* __restrict__ out) {
   const int row = blockIdx.x;
   const size_t stride = (size_t)rows * ncols;
   const float* pr = P + (size_t)row * ncols;
   T* o = out + (size_t)row * ncols;
   const int p0 = pos[row];
-  for (int p = threadIdx.x; p < rope_cols / 2; p += kThreads) {
-    const int c1 = (p / 64) * 128 + (p % 64), c2 = c1 + 64;
-    float x = 0.f, y = 0.f;
-    for (int k = 0; k < ksplit; ++k) {
-      x += pr[k * stride + c1];
-      y += pr[k * stride + c2];
+  // rotated pairs: chunk q covers dims i0..i0+7 and i0+64..i0+71 of a head
+  const int npairs = rope_cols / 16;
+  for (int q = threadIdx.x; q < npairs; q += kThreads) {
+    const int i0 = (q % 8) * 8;
+    const int c1 = (q / 8) * 128 + i0, c2 = c1 + 64;
+    float x[8] = {0, 0, 0, 0, 0, 0, 0, 0}, y[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    sum_parts<KS>(pr + c1, stride, x);
+    sum_parts<KS>(pr + c2, stride, y);
+    float cv[8], sv[8];
+    const float4* cp = reinterpret_cast<const float4*>(cs + (size_t)p0 * 64 + i0);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 t = cp[u];
+      cv[2 * u] = t.x; sv[2 * u] = t.y; cv[2 * u + 1] = t.z; sv[2 * u + 1] = t.w;
     }
-    const float2 c = cs[(size_t)p0 * 64 + (p % 64)];
-    o[c1] = Fmt::store(x * c.x - y * c.y);
-    o[c2] = Fmt::store(y * c.x + x * c.y);
+    float a[8], b[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      a[i] = x[i] * cv[i] - y[i] * sv[i];
+      b[i] = y[i] * cv[i] + x[i] * sv[i];
+    }
+    store8<Fmt>(o + c1, a);
+    store8<Fmt>(o + c2, b);
   }
-  for (int c = rope_cols + threadIdx.x; c < ncols; c += kThreads) {
-    float x = 0.f;
-    for (int k = 0; k < ksplit; ++k) x += pr[k * stride + c];
-    o[c] = Fmt::store(x);
+  for (int c = rope_cols + threadIdx.x * 8; c < ncols; c += kThreads * 8) {
+    float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    sum_parts<KS>(pr + c, stride, x);
+    store8<Fmt>(o + c, x);
   }
 }
 
-template <typename Fmt, typename T = typename Fmt::st>
+template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
-reduce_swiglu_kernel(const float* __restrict__ P, int ksplit, int rows,
-                     int ffn, T* __restrict__ out) {
+reduce_swiglu_kernel(const float* __restrict__ P, int rows, int ffn,
+                     T* __restrict__ out) {
   const int row = blockIdx.x;
   const size_t ld = (size_t)2 * ffn;
   const size_t stride = (size_t)rows * ld;
   const float* pr = P + (size_t)row * ld;
-  for (int c = threadIdx.x; c < ffn; c += kThreads) {
-    float g = 0.f, u = 0.f;
-    for (int k = 0; k < ksplit; ++k) {
-      g += pr[k * stride + c];
-      u += pr[k * stride + ffn + c];
-    }
-    out[(size_t)row * ffn + c] = Fmt::store(g / (1.0f + __expf(-g)) * u);
+  for (int c = threadIdx.x * 8; c < ffn; c += kThreads * 8) {
+    float g[8] = {0, 0, 0, 0, 0, 0, 0, 0}, u[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    sum_parts<KS>(pr + c, stride, g);
+    sum_parts<KS>(pr + ffn + c, stride, u);
+    float h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = g[i] / (1.0f + __expf(-g[i])) * u[i];
+    store8<Fmt>(out + (size_t)row * ffn + c, h);
   }
 }
 
@@ -432,14 +519,24 @@ int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
     else { using F = BF16S; F_BODY; }                                       \
   } while (0)
 
+#define DISPATCH_KS(ksplit, BODY)                                           \
+  do {                                                                      \
+    switch (ksplit) {                                                       \
+      case 2: { constexpr int KS = 2; BODY; } break;                        \
+      case 4: { constexpr int KS = 4; BODY; } break;                        \
+      case 8: { constexpr int KS = 8; BODY; } break;                        \
+      default: return set_error(DAVET_EINVAL, "split-K: ksplit must be 2, 4 or 8"); \
+    }                                                                       \
+  } while (0)
+
 int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,
                            int d, float* X, const float* gain, float eps,
                            void* A, hipStream_t s) {
   if (rows <= 0) return DAVET_OK;
   ProfScope ps(KC_RMSNORM, s);
-  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_add_norm_kernel<F>, dim3(rows),
-                                       dim3(kThreads), 0, s, P, ksplit, rows,
-                                       d, X, gain, eps, (F::st*)A));
+  DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
+      (reduce_add_norm_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P,
+      rows, d, X, gain, eps, (F::st*)A)));
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -448,11 +545,12 @@ int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
                              int ncols, int rope_cols, const int32_t* pos,
                              const float* cs, void* out, hipStream_t s) {
   if (rows <= 0) return DAVET_OK;
+  if (rope_cols % 128 || ncols % 8)
+    return set_error(DAVET_ESHAPE, "reduce_store_rope: column counts");
   ProfScope ps(KC_ROPE, s);
-  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_store_rope_kernel<F>, dim3(rows),
-                                       dim3(kThreads), 0, s, P, ksplit, rows,
-                                       ncols, rope_cols, pos,
-                                       (const float2*)cs, (F::st*)out));
+  DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
+      (reduce_store_rope_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P,
+      rows, ncols, rope_cols, pos, (const float2*)cs, (F::st*)out)));
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
@@ -460,13 +558,15 @@ int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
 int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
                          int ffn, void* out, hipStream_t s) {
   if (rows <= 0) return DAVET_OK;
+  if (ffn % 8) return set_error(DAVET_ESHAPE, "reduce_swiglu: ffn % 8 != 0");
   ProfScope ps(KC_MISC, s);
-  DISPATCH16(dtype, hipLaunchKernelGGL(reduce_swiglu_kernel<F>, dim3(rows),
-                                       dim3(kThreads), 0, s, P, ksplit, rows,
-                                       ffn, (F::st*)out));
+  DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
+      (reduce_swiglu_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P, rows,
+      ffn, (F::st*)out)));
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
+#undef DISPATCH_KS
 
 int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const void* embed, const int32_t* prompt_ids,

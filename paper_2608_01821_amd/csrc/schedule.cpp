@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <vector>
 
@@ -13,7 +14,16 @@
 
 namespace davet {
 void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
-                      int64_t L, size_t* conf_off, size_t* argmax_off);
+                      int64_t L, size_t* conf_off, size_t* argmax_off,
+                      size_t* rope_off);
+int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
+                      int32_t n_seqs, const void* const* view_ptrs,
+                      const int32_t* n_view, const int32_t* prompt_ids,
+                      const int32_t* cu_prompt, const int32_t* resp_ids,
+                      const uint8_t* resp_masked, int32_t L, float* conf_out,
+                      int32_t* argmax_out, float* logits_out, void* workspace,
+                      size_t ws_bytes, const float* rope_cs,
+                      hipStream_t stream);
 }
 
 extern "C" int davet_run_schedule(
@@ -46,7 +56,7 @@ extern "C" int davet_run_schedule(
   // views: level pointers and sizes per sequence
   std::vector<const void*> lvl_ptr((size_t)n_seqs * K);
   std::vector<int32_t> lvl_n((size_t)n_seqs * K);
-  int64_t max_tokens = 0;
+  int64_t max_tokens = 0, max_len = 0;
   for (int s = 0; s < n_seqs; ++s) {
     const davet_view_geom& g = geoms[s];
     DAVET_CHECK_ARG(g.K == K && g.d == cfg->d && g.dtype == cfg->dtype,
@@ -57,7 +67,10 @@ extern "C" int davet_run_schedule(
     for (int l = 0; l < K; ++l)
       lvl_ptr[(size_t)s * K + l] =
           l == K - 1 ? visual[s] : view_bufs[(size_t)s * (K - 1) + l];
-    max_tokens += lvl_n[(size_t)s * K + K - 1] + (cu_prompt[s + 1] - cu_prompt[s]) + L;
+    const int64_t len =
+        lvl_n[(size_t)s * K + K - 1] + (cu_prompt[s + 1] - cu_prompt[s]) + L;
+    max_tokens += len;
+    max_len = std::max(max_len, len);
   }
   if (fixed_levels)
     for (int i = 0; i < n_seqs * T; ++i)
@@ -70,9 +83,18 @@ extern "C" int davet_run_schedule(
   }
   DAVET_CHECK_ARG(ws_bytes >= need, DAVET_ENOMEM,
                   "davet_run_schedule: workspace smaller than the full-view size");
-  size_t conf_off = 0, am_off = 0;
-  schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off);
+  size_t conf_off = 0, am_off = 0, rope_off = 0;
+  schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off, &rope_off);
   char* ws = static_cast<char*>(workspace);
+
+  // rotary table for every position of the longest sequence, once per loop
+  // (a step's sequences are never longer than at the full view)
+  float* rope = reinterpret_cast<float*>(ws + rope_off);
+  {
+    int rc = launch_rope_table((int)max_len, cfg->head_dim, cfg->rope_theta,
+                               rope, stream);
+    if (rc) return rc;
+  }
 
   // a1: evidence views, once per sample
   for (int s = 0; s < n_seqs; ++s) {
@@ -124,9 +146,10 @@ extern "C" int davet_run_schedule(
                              : reinterpret_cast<float*>(ws + conf_off);
     int32_t* am = argmax_trace ? argmax_trace + (size_t)(t - 1) * n_seqs * L
                                : reinterpret_cast<int32_t*>(ws + am_off);
-    int rc = davet_denoise_step(cfg, w, n_seqs, vptr.data(), nview.data(),
-                                prompt_ids, cu_prompt, resp_ids, resp_masked, L,
-                                conf, am, nullptr, workspace, ws_bytes, stream);
+    int rc = denoise_step_impl(cfg, w, n_seqs, vptr.data(), nview.data(),
+                               prompt_ids, cu_prompt, resp_ids, resp_masked, L,
+                               conf, am, nullptr, workspace, ws_bytes, rope,
+                               stream);
     if (rc) return rc;
     rc = davet_unmask(n_seqs, L, k, conf, am, resp_ids, resp_masked, nullptr,
                       stream);

@@ -26,6 +26,7 @@ struct Layout {
   size_t conf, argmax;                 // run_schedule scratch
   size_t X, A, QKV, O, H, rope, pos, list, Hm, pmax, psum, parg, logits;
   size_t part;                         // split-K partial tiles (16-bit path)
+  size_t rope_sched;                   // run_schedule's rotary table (last)
   size_t total;
 };
 
@@ -83,9 +84,16 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
     o.logits = take((size_t)rows * c.vocab * 4);
   }
   o.part = take(partial_bytes(c, tokens));
+  // Every region above grows with the token count, so a step with fewer
+  // tokens than the workspace was sized for never reaches this one: the
+  // schedule loop keeps its rotary table here for all its steps.
+  o.rope_sched = take((size_t)tokens * (c.head_dim / 2) * 8);
   o.total = p;
   return o;
 }
+
+// null counts as aligned (optional vectors)
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 static int check_cfg(const davet_model_cfg* c) {
   DAVET_CHECK_ARG(c, DAVET_EINVAL, "model cfg is null");
@@ -120,10 +128,12 @@ int workspace_layout_bytes(const davet_model_cfg* c, int64_t tokens,
 
 // Used by run_schedule to reach its scratch region.
 void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
-                      int64_t L, size_t* conf_off, size_t* argmax_off) {
+                      int64_t L, size_t* conf_off, size_t* argmax_off,
+                      size_t* rope_off) {
   const Layout o = make_layout(*c, tokens, seqs, L);
   *conf_off = o.conf;
   *argmax_off = o.argmax;
+  *rope_off = o.rope_sched;
 }
 
 }  // namespace davet
@@ -141,6 +151,17 @@ extern "C" int davet_workspace_bytes(const davet_model_cfg* cfg,
   return workspace_layout_bytes(cfg, max_tokens, max_seqs, L, bytes);
 }
 
+namespace davet {
+int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
+                      int32_t n_seqs, const void* const* view_ptrs,
+                      const int32_t* n_view, const int32_t* prompt_ids,
+                      const int32_t* cu_prompt, const int32_t* resp_ids,
+                      const uint8_t* resp_masked, int32_t L, float* conf_out,
+                      int32_t* argmax_out, float* logits_out, void* workspace,
+                      size_t ws_bytes, const float* rope_cs,
+                      hipStream_t stream);
+}  // namespace davet
+
 extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
                                   const davet_weights* w, int32_t n_seqs,
                                   const void* const* view_ptrs,
@@ -152,6 +173,23 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
                                   float* conf_out, int32_t* argmax_out,
                                   float* logits_out, void* workspace,
                                   size_t ws_bytes, hipStream_t stream) {
+  return davet::denoise_step_impl(cfg, w, n_seqs, view_ptrs, n_view,
+                                  prompt_ids, cu_prompt, resp_ids, resp_masked,
+                                  L, conf_out, argmax_out, logits_out,
+                                  workspace, ws_bytes, nullptr, stream);
+}
+
+// rope_cs: a rotary table already holding every position this step uses
+// (the schedule loop's); null: build it in the step's own region.
+int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
+                             int32_t n_seqs, const void* const* view_ptrs,
+                             const int32_t* n_view, const int32_t* prompt_ids,
+                             const int32_t* cu_prompt, const int32_t* resp_ids,
+                             const uint8_t* resp_masked, int32_t L,
+                             float* conf_out, int32_t* argmax_out,
+                             float* logits_out, void* workspace,
+                             size_t ws_bytes, const float* rope_cs,
+                             hipStream_t stream) {
   using namespace davet;
   int rc = check_cfg(cfg);
   if (rc) return rc;
@@ -164,7 +202,16 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
     const davet_layer_weights& lw = w->layers[l];
     DAVET_CHECK_ARG(lw.wqkv && lw.wo && lw.wg && lw.wu && lw.wd, DAVET_EINVAL,
                     "davet_denoise_step: null layer weight");
+    DAVET_CHECK_ARG(aligned16(lw.wqkv) && aligned16(lw.wo) && aligned16(lw.wg) &&
+                        aligned16(lw.wu) && aligned16(lw.wd) &&
+                        aligned16(lw.attn_norm) && aligned16(lw.ffn_norm),
+                    DAVET_EINVAL,
+                    "davet_denoise_step: layer weights must be 16-byte aligned");
   }
+  DAVET_CHECK_ARG(aligned16(w->embed) && aligned16(w->head) &&
+                      aligned16(w->final_norm),
+                  DAVET_EINVAL,
+                  "davet_denoise_step: weights must be 16-byte aligned");
   DAVET_CHECK_ARG(n_seqs >= 1 && n_seqs <= DAVET_MAX_SEQS, DAVET_ESHAPE,
                   "davet_denoise_step: n_seqs out of range [1, 64]");
   DAVET_CHECK_ARG(L >= 1 && L <= DAVET_MAX_RESP, DAVET_ESHAPE,
@@ -188,6 +235,8 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
                     "davet_denoise_step: negative view length");
     DAVET_CHECK_ARG(n_view[s] == 0 || view_ptrs[s], DAVET_EINVAL,
                     "davet_denoise_step: null view pointer");
+    DAVET_CHECK_ARG(aligned16(view_ptrs[s]), DAVET_EINVAL,
+                    "davet_denoise_step: view pointers must be 16-byte aligned");
     const int plen = cu_prompt[s + 1] - cu_prompt[s];
     DAVET_CHECK_ARG(plen >= 0, DAVET_ESHAPE,
                     "davet_denoise_step: cu_prompt must be non-decreasing");
@@ -218,7 +267,7 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   void* QKV = ws + lay.QKV;
   void* O = ws + lay.O;
   void* H = ws + lay.H;
-  float* rope = reinterpret_cast<float*>(ws + lay.rope);
+  const float* rope = rope_cs ? rope_cs : reinterpret_cast<float*>(ws + lay.rope);
   int32_t* pos = reinterpret_cast<int32_t*>(ws + lay.pos);
   float* part = reinterpret_cast<float*>(ws + lay.part);
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
@@ -230,7 +279,9 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   hipStream_t s = stream;
 
 #define RUN(x) do { int rc_ = (x); if (rc_) return rc_; } while (0)
-  RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta, rope, s));
+  if (!rope_cs)
+    RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta,
+                          reinterpret_cast<float*>(ws + lay.rope), s));
   RUN(launch_head_prep(sp, resp_masked, list, conf_out, argmax_out, s));
   const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
   RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,

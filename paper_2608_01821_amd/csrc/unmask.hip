@@ -10,43 +10,62 @@
 namespace davet {
 namespace {
 
-__device__ __forceinline__ float rank_key(float c) {
-  return (c != c) ? -INFINITY : c;
+// Rank key of a position: NaN ranks as -inf and -0 as +0 (equal floats tie
+// and fall back to the position), encoded so that unsigned order is
+// (confidence descending, position ascending); committed positions get the
+// largest key and are never counted.
+__device__ __forceinline__ uint64_t rank_code(float c, int i) {
+  if (c != c) c = -INFINITY;
+  if (c == 0.f) c = 0.f;
+  uint32_t u = __float_as_uint(c);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);   // ascending float order
+  return ((uint64_t)(~u) << 32) | (uint32_t)i;
 }
+
+constexpr int kPer = DAVET_MAX_RESP / 256;   // positions per thread
 
 __global__ void __launch_bounds__(256)
 unmask_kernel(int L, int k, const float* __restrict__ conf,
               const int32_t* __restrict__ argmax, int32_t* __restrict__ ids,
               uint8_t* __restrict__ masked, int32_t* __restrict__ selected) {
-  __shared__ float key[DAVET_MAX_RESP];
-  __shared__ uint8_t msk[DAVET_MAX_RESP];
-  __shared__ int cnt;
+  __shared__ uint64_t code[DAVET_MAX_RESP];
+  __shared__ int wcnt[4];
   const int s = blockIdx.x;
   const size_t base = (size_t)s * L;
-  if (threadIdx.x == 0) cnt = 0;
-  __syncthreads();
+  uint64_t mine[kPer];
   int local = 0;
-  for (int i = threadIdx.x; i < L; i += blockDim.x) {
-    const uint8_t m = masked[base + i] != 0;
-    msk[i] = m;
-    key[i] = rank_key(conf[base + i]);
-    local += m;
-  }
-  atomicAdd(&cnt, local);
-  __syncthreads();
-  const int kt = min(k, cnt);
-  for (int i = threadIdx.x; i < L; i += blockDim.x) {
-    if (!msk[i]) continue;
-    const float ki = key[i];
-    int rank = 0;
-    for (int j = 0; j < L; ++j) {
-      const float kj = key[j];
-      rank += msk[j] && (kj > ki || (kj == ki && j < i));
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int i = threadIdx.x + q * 256;
+    mine[q] = ~0ull;
+    if (i < L) {
+      if (masked[base + i]) {
+        mine[q] = rank_code(conf[base + i], i);
+        ++local;
+      }
+      code[i] = mine[q];
     }
-    if (rank < kt) {
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) local += __shfl_xor(local, o, 64);
+  if ((threadIdx.x & 63) == 0) wcnt[threadIdx.x >> 6] = local;
+  __syncthreads();
+  const int kt = min(k, wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3]);
+  int rank[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) rank[q] = 0;
+  for (int j = 0; j < L; ++j) {
+    const uint64_t cj = code[j];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) rank[q] += cj < mine[q];
+  }
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int i = threadIdx.x + q * 256;
+    if (i < L && mine[q] != ~0ull && rank[q] < kt) {
       ids[base + i] = argmax[base + i];
       masked[base + i] = 0;
-      if (selected) selected[(size_t)s * k + rank] = i;
+      if (selected) selected[(size_t)s * k + rank[q]] = i;
     }
   }
   if (selected)
