@@ -4,16 +4,21 @@
 // every key of the same sequence; sequences never mix.
 //
 // 16-bit path (bf16 or fp16 operands), head_dim 128, CDNA4 matrix cores.  A
-// workgroup of 4 wavefronts owns 128 queries of one head; each wavefront owns
-// 32 queries.  Keys stream in tiles of 64 staged in LDS: K row-major, V
-// transposed.  Per tile a wavefront computes S^T = K Q^T (2 x 8
-// v_mfma_f32_32x32x16 ops), so every lane holds the scores of ONE query: the
-// online-softmax rescale is a per-lane scalar and the probabilities, rounded
-// to 16 bits, are already laid out as the B operand of O^T += V^T P^T (4 x 4
-// MFMAs) -- no LDS round trip for P.  Scores,
-// running max and normaliser stay in fp32 (exp2 with log2(e) folded into the
-// 1/sqrt(D) scale).  Ragged tails: keys past the sequence end score -inf;
-// queries past it are computed on clamped rows and never stored.
+// workgroup owns 128 queries of one head and runs SPLIT groups of 4
+// wavefronts; group g takes the key tiles g, g + SPLIT, ... and each of its
+// wavefronts owns 32 queries.  Keys stream in tiles of 64 staged in LDS (K
+// row-major, V transposed); the next tile of a group is fetched into registers
+// while the current one feeds the matrix cores.  Per tile a wavefront computes
+// S^T = K Q^T (2 x 8 v_mfma_f32_32x32x16 ops), so every lane holds the scores
+// of ONE query: the online-softmax rescale is a per-lane scalar and the
+// probabilities, rounded to 16 bits, are already laid out as the B operand of
+// O^T += V^T P^T (4 x 4 MFMAs) -- no LDS round trip for P.  Scores, running
+// max and normaliser stay in fp32 (exp2 with log2(e) folded into the
+// 1/sqrt(D) scale).  The groups' partial (max, normaliser, O) are merged
+// through LDS at the end.  Ragged tails: keys past the sequence end score
+// -inf; queries past it are computed on clamped rows and never stored.
+// Workgroup ids are remapped so the query tiles of a head share an XCD (and
+// its L2 copy of that head's keys and values).
 
 #include "common.h"
 
@@ -25,6 +30,14 @@ constexpr int QT = 128;           // queries per workgroup
 constexpr int KT = 64;            // keys per tile
 constexpr int K_STRIDE = HD + 8;  // 272-byte K rows
 constexpr int V_STRIDE = KT + 4;  // 136-byte V^T rows (conflict-free b64 reads)
+constexpr int GROUP_LDS = KT * K_STRIDE + HD * V_STRIDE;   // uint16 per group
+
+__device__ __forceinline__ int remap_xcd_attn(int bid, int nwg) {
+  const int full = nwg & ~7;
+  if (bid >= full) return bid;
+  const int per = full >> 3;
+  return (bid & 7) * per + (bid >> 3);
+}
 
 __device__ __forceinline__ void locate_tile(const SeqPack& sp, int tile,
                                             int qtile, int& s, int& qt) {
@@ -40,25 +53,34 @@ __device__ __forceinline__ void locate_tile(const SeqPack& sp, int tile,
   qt = tile - acc;
 }
 
-template <typename Fmt>
-__global__ void __launch_bounds__(256, 1)
+template <typename Fmt, int SPLIT>
+__global__ void __launch_bounds__(256 * SPLIT, 1)
 attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
-              SeqPack sp, int n_heads, float scale_log2) {
+              SeqPack sp, int n_heads, int n_tiles, float scale_log2) {
   using v8 = typename Fmt::v8;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * K_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * V_STRIDE];
+  // SPLIT groups' K/V^T tiles; after the loop the same bytes hold the merge
+  // (merge: O as [4 waves][4][16][64 lanes] floats, then max and normaliser
+  // as [4][64] floats each)
+  constexpr int MERGE_U16 = 2 * (QT * HD + 2 * 256);
+  constexpr int LDS_U16 = SPLIT * GROUP_LDS > MERGE_U16 ? SPLIT * GROUP_LDS
+                                                        : MERGE_U16;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[LDS_U16];
+  const int logical = remap_xcd_attn(blockIdx.x, gridDim.x);
+  const int h = logical / n_tiles;
   int s, qt;
-  locate_tile(sp, blockIdx.x, QT, s, qt);
-  const int h = blockIdx.y;
+  locate_tile(sp, logical % n_tiles, QT, s, qt);
   const int d = n_heads * HD;
   const size_t ld = (size_t)3 * d;
   const int row0 = sp.row0[s];
   const int N = sp.row0[s + 1] - row0;
   const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
+  const int grp = t >> 8, tg = t & 255;
+  const int lane = t & 63, wave = (t >> 6) & 3;
   const int l32 = lane & 31, hh = lane >> 5;
   const int q = qt * QT + wave * 32 + l32;         // this lane's query
   const int qc = min(q, N - 1);
+  uint16_t* Ks = smem + grp * GROUP_LDS;
+  uint16_t* Vt = Ks + KT * K_STRIDE;
 
   // Q^T fragments (B operand): 8 k-steps of 16 head dims
   v8 qf[HD / 16];
@@ -78,101 +100,161 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
 
   const uint16_t* kbase = qkv + (size_t)row0 * ld + d + (size_t)h * HD;
   const uint16_t* vbase = qkv + (size_t)row0 * ld + 2 * d + (size_t)h * HD;
-  const int n_kt = (N + KT - 1) / KT;
-  for (int kb = 0; kb < n_kt; ++kb) {
+  constexpr int KI = KT * HD / 8 / 256;     // 16-byte K loads per thread
+  constexpr int VI = KT * HD / 16 / 256;    // key pairs of V per thread
+  u32x4 kr[KI], va[VI], vb[VI];
+  auto fetch = [&](int kb) {
     const int k0 = kb * KT;
-    // ---- stage K (row-major) and V (transposed) tiles in LDS
 #pragma unroll
-    for (int it = 0; it < KT * HD / 8 / 256; ++it) {
-      const int w = t + it * 256;
-      const int key = w >> 4, ch = w & 15;
-      const int gk = min(k0 + key, N - 1);
-      *reinterpret_cast<u32x4*>(&Ks[key * K_STRIDE + ch * 8]) =
-          *reinterpret_cast<const u32x4*>(kbase + (size_t)gk * ld + ch * 8);
+    for (int it = 0; it < KI; ++it) {
+      const int w = tg + it * 256;
+      const int gk = min(k0 + (w >> 4), N - 1);
+      kr[it] = *reinterpret_cast<const u32x4*>(kbase + (size_t)gk * ld + (w & 15) * 8);
     }
 #pragma unroll
-    for (int it = 0; it < KT * HD / 16 / 256; ++it) {
-      const int w = t + it * 256;
+    for (int it = 0; it < VI; ++it) {
+      const int w = tg + it * 256;
       const int kp = w >> 4, dc = w & 15;
       const int g0 = min(k0 + 2 * kp, N - 1), g1 = min(k0 + 2 * kp + 1, N - 1);
-      const u32x4 a = *reinterpret_cast<const u32x4*>(vbase + (size_t)g0 * ld + dc * 8);
-      const u32x4 b = *reinterpret_cast<const u32x4*>(vbase + (size_t)g1 * ld + dc * 8);
+      va[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)g0 * ld + dc * 8);
+      vb[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)g1 * ld + dc * 8);
+    }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int it = 0; it < KI; ++it) {
+      const int w = tg + it * 256;
+      *reinterpret_cast<u32x4*>(&Ks[(w >> 4) * K_STRIDE + (w & 15) * 8]) = kr[it];
+    }
+#pragma unroll
+    for (int it = 0; it < VI; ++it) {
+      const int w = tg + it * 256;
+      const int kp = w >> 4, dc = w & 15;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = (a[e] & 0xffffu) | (b[e] << 16);
-        const uint32_t hi = (a[e] >> 16) | (b[e] & 0xffff0000u);
+        const uint32_t lo = (va[it][e] & 0xffffu) | (vb[it][e] << 16);
+        const uint32_t hi = (va[it][e] >> 16) | (vb[it][e] & 0xffff0000u);
         *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * e) * V_STRIDE + 2 * kp]) = lo;
         *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * e + 1) * V_STRIDE + 2 * kp]) = hi;
       }
     }
-    __syncthreads();
+  };
 
-    // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
-    f32x16 sc[2];
+  const int n_kt = (N + KT - 1) / KT;
+  const int n_it = (n_kt + SPLIT - 1) / SPLIT;     // same for every group
+  if (grp < n_kt) fetch(grp);
+  for (int it = 0; it < n_it; ++it) {
+    const int kb = it * SPLIT + grp;
+    const bool have = kb < n_kt;
+    if (have) stash();
+    __syncthreads();
+    if (kb + SPLIT < n_kt) fetch(kb + SPLIT);      // in flight during compute
+    if (have) {
+      const int k0 = kb * KT;
+      // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
+      f32x16 sc[2];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+      for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
+        for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < HD / 16; ++ks) {
-        const v8 kf = __builtin_bit_cast(
-            v8, *reinterpret_cast<const u32x4*>(
-                    &Ks[(mt * 32 + l32) * K_STRIDE + ks * 16 + hh * 8]));
-        sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
+        for (int ks = 0; ks < HD / 16; ++ks) {
+          const v8 kf = __builtin_bit_cast(
+              v8, *reinterpret_cast<const u32x4*>(
+                      &Ks[(mt * 32 + l32) * K_STRIDE + ks * 16 + hh * 8]));
+          sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
+        }
+      }
+      // ---- online softmax for this lane's query over its 32 keys + partner's.
+      // The running max is kept on raw scores (the scale is positive), so
+      // each probability costs one fma and one exp2: 2^(s*scale - m*scale).
+      if (k0 + KT > N) {                 // ragged last tile only
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = k0 + mt * 32 + (e >> 2) * 8 + hh * 4 + (e & 3);
+            if (key >= N) sc[mt][e] = -INFINITY;
+          }
+      }
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sc[mt][e]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float m_new = fmaxf(m_run, tmax);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
+      const float neg_m = -m_new * scale_log2;
+      float psum = 0.f;
+      uint16_t pb[4][8];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[mt][e], scale_log2, neg_m));
+          psum += p;
+          pb[mt * 2 + (e >> 3)][e & 7] = Fmt::store(p);
+        }
+      psum += __shfl_xor(psum, 32, 64);
+      l_run = l_run * alpha + psum;
+      m_run = m_new;
+      // rescale the accumulator unless no lane's maximum moved
+      if (__any(alpha != 1.0f)) {
+#pragma unroll
+        for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+      }
+
+      // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
+#pragma unroll
+      for (int ps = 0; ps < 4; ++ps) {
+        const int kl = ps * 16 + hh * 4;
+#pragma unroll
+        for (int dt = 0; dt < HD / 32; ++dt) {
+          const uint16_t* vr = &Vt[(dt * 32 + l32) * V_STRIDE + kl];
+          const u32x2 v0 = *reinterpret_cast<const u32x2*>(vr);
+          const u32x2 v1 = *reinterpret_cast<const u32x2*>(vr + 8);
+          u32x4 vv;
+          vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
+          u32x4 pw;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            pw[u] = (uint32_t)pb[ps][2 * u] | ((uint32_t)pb[ps][2 * u + 1] << 16);
+          o[dt] = Fmt::mfma32(__builtin_bit_cast(v8, vv),
+                              __builtin_bit_cast(v8, pw), o[dt]);
+        }
       }
     }
-    // ---- online softmax for this lane's query over its 32 keys + partner's 32
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = k0 + mt * 32 + (e >> 2) * 8 + hh * 4 + (e & 3);
-        const float v = key < N ? sc[mt][e] * scale_log2 : -INFINITY;
-        sc[mt][e] = v;
-        tmax = fmaxf(tmax, v);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = exp2f(m_run - m_new);
-    float psum = 0.f;
-    uint16_t pb[4][8];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = exp2f(sc[mt][e] - m_new);
-        psum += p;
-        pb[mt * 2 + (e >> 3)][e & 7] = Fmt::store(p);
-      }
-    psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+    __syncthreads();
+  }
 
-    // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
+  if constexpr (SPLIT == 2) {
+    // group 1 hands (max, normaliser, O) of each query to group 0
+    float* mo = reinterpret_cast<float*>(smem);          // [4][4][16][64]
+    float* ml = mo + QT * HD;                              // [4][64] x 2
+    if (grp == 1) {
 #pragma unroll
-    for (int ps = 0; ps < 4; ++ps) {
-      const int kbase_l = ps * 16 + hh * 4;
+      for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
-      for (int dt = 0; dt < HD / 32; ++dt) {
-        const uint16_t* vr = &Vt[(dt * 32 + l32) * V_STRIDE + kbase_l];
-        const u32x2 v0 = *reinterpret_cast<const u32x2*>(vr);
-        const u32x2 v1 = *reinterpret_cast<const u32x2*>(vr + 8);
-        u32x4 vv;
-        vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
-        u32x4 pw;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          pw[q] = (uint32_t)pb[ps][2 * q] | ((uint32_t)pb[ps][2 * q + 1] << 16);
-        o[dt] = Fmt::mfma32(__builtin_bit_cast(v8, vv),
-                            __builtin_bit_cast(v8, pw), o[dt]);
-      }
+        for (int e = 0; e < 16; ++e)
+          mo[((wave * 4 + dt) * 16 + e) * 64 + lane] = o[dt][e];
+      ml[wave * 64 + lane] = m_run;
+      ml[256 + wave * 64 + lane] = l_run;
     }
     __syncthreads();
+    if (grp == 1) return;
+    const float m1 = ml[wave * 64 + lane], l1 = ml[256 + wave * 64 + lane];
+    const float mm = fmaxf(m_run, m1);
+    const float a0 = exp2f((m_run - mm) * scale_log2);
+    const float a1 = exp2f((m1 - mm) * scale_log2);
+    l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+    for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        o[dt][e] = o[dt][e] * a0 + mo[((wave * 4 + dt) * 16 + e) * 64 + lane] * a1;
   }
 
   if (q < N) {
@@ -244,12 +326,13 @@ int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
   if (tiles == 0) return DAVET_OK;
   ProfScope ps(KC_ATTN, s);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
+  const dim3 grid(tiles * n_heads);
   if (dtype == DAVET_F16)
-    hipLaunchKernelGGL(attn16_kernel<F16>, dim3(tiles, n_heads), dim3(256), 0,
-                       s, qkv, o, sp, n_heads, scale_log2);
+    hipLaunchKernelGGL((attn16_kernel<F16, 2>), grid, dim3(512), 0, s, qkv, o,
+                       sp, n_heads, tiles, scale_log2);
   else
-    hipLaunchKernelGGL(attn16_kernel<BF16>, dim3(tiles, n_heads), dim3(256), 0,
-                       s, qkv, o, sp, n_heads, scale_log2);
+    hipLaunchKernelGGL((attn16_kernel<BF16, 2>), grid, dim3(512), 0, s, qkv,
+                       o, sp, n_heads, tiles, scale_log2);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
