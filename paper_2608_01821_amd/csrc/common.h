@@ -197,7 +197,11 @@ GemmPlan plan_gemm16(int M, int N, int K);
 int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
                   const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
                   int K, int ldc, const int32_t* pos, const float* cs,
-                  int rope_cols, float* partials, int cls, hipStream_t s);
+                  int rope_cols, float* partials, size_t partial_cap, int cls,
+                  hipStream_t s);
+// Largest fp32 split-K partial buffer (bytes) plan_gemm16 may ask for with
+// M <= max_M rows of an N x K product.
+size_t gemm16_partial_bound(int max_M, int N, int K);
 // Split-K reductions (fixed summation order over the splits):
 //   X[r] += sum_s P[s][r]; then A[r] = RMSNorm(X[r]) * gain when A is given
 int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,

@@ -499,12 +499,35 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 
 }  // namespace
 
-// Kernel choice measured on MI355X over the workload shapes (d = 4096,
-// ffn = 12288, 209..18020 tokens): 128 x 128 tiles with 128-byte slabs and two
-// workgroups per CU win up to ~2-3K rows; 256 x 256 tiles with 8 wavefronts
-// win above (50-55% of the fp16 matrix peak).  Narrow-N products (the output
-// and down projections) split K until the grid fills the 256 CUs.
-GemmPlan plan_gemm16(int M, int N, int K) {
+// Kernel choice.  For the projections of a d = 4096, ffn = 12288 layer the
+// plan is a table measured on MI355X with the weights and activations cold in
+// the last-level cache (as inside a denoising step), by token-count bucket:
+// the fastest (tile variant, K split) of a sweep over every variant and split
+// in {1, 2, 4, 8}, the split-K reduction included.  Bucket upper bounds:
+constexpr int kBuckets[] = {300, 470, 700, 1100, 1700, 2600, 1 << 30};
+constexpr int kNB = 7;
+struct TableShape { int N, K; GemmPlan plan[kNB]; };
+constexpr TableShape kTable[] = {
+    // QKV: N = 3d, K = d
+    {12288, 4096, {{8, 4, 0}, {8, 2, 0}, {6, 1, 0}, {8, 1, 0}, {6, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    // output projection: N = d, K = d
+    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
+    // gate + up: N = 2 ffn, K = d
+    {24576, 4096, {{6, 1, 0}, {8, 1, 0}, {6, 1, 0}, {6, 1, 0}, {6, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    // down projection: N = d, K = ffn
+    {4096, 12288, {{6, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
+};
+
+static const TableShape* table_shape(int N, int K) {
+  for (const TableShape& t : kTable)
+    if (t.N == N && t.K == K) return &t;
+  return nullptr;
+}
+
+// Other shapes: 128 x 128 tiles with 128-byte slabs and two workgroups per CU
+// up to ~2-3K rows, 256 x 256 tiles with 8 wavefronts above; narrow-N
+// products split K until the grid fills the 256 CUs (tiles * ksplit < 512).
+static GemmPlan plan_generic(int M, int N, int K) {
   GemmPlan p{};
   const bool big = M >= (N >= 16384 ? 2048 : 3000);
   p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 8 : (K % 64 == 0 ? 6 : 0);
@@ -518,11 +541,41 @@ GemmPlan plan_gemm16(int M, int N, int K) {
   return p;
 }
 
+GemmPlan plan_gemm16(int M, int N, int K) {
+  if (const TableShape* t = table_shape(N, K)) {
+    int b = 0;
+    while (M >= kBuckets[b]) ++b;
+    return t->plan[b];
+  }
+  return plan_generic(M, N, K);
+}
+
+// Largest split-K partial buffer (bytes) any M <= max_M needs.  Table shapes:
+// the bound is reached at the top of a bucket (or at max_M).  Other shapes:
+// tiles * ksplit < 512 caps it at 512 tiles of at most 256 x 256.
+size_t gemm16_partial_bound(int max_M, int N, int K) {
+  size_t best = 0;
+  auto at = [&](int m) {
+    if (m < 1) return;
+    const GemmPlan p = plan_gemm16(m, N, K);
+    if (p.ksplit > 1) best = std::max(best, (size_t)p.ksplit * m * N * 4);
+  };
+  if (table_shape(N, K)) {
+    for (int b = 0; b < kNB; ++b) at(std::min(max_M, kBuckets[b] - 1));
+    at(max_M);
+    return best;
+  }
+  return (size_t)512 * 256 * 256 * 4;
+}
+
 int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
                   const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
                   int K, int ldc, const int32_t* pos, const float* cs,
-                  int rope_cols, float* partials, int cls, hipStream_t s) {
+                  int rope_cols, float* partials, size_t partial_cap, int cls,
+                  hipStream_t s) {
   if (M <= 0) return DAVET_OK;
+  if (plan.ksplit > 1 && (size_t)plan.ksplit * M * N * 4 > partial_cap)
+    return set_error(DAVET_ENOMEM, "gemm16: split-K partials exceed the workspace");
   if (N % variant_bn(plan.tile) || K % variant_bk(plan.tile) ||
       (plan.ksplit > 1 && (K / variant_bk(plan.tile)) < plan.ksplit))
     return set_error(DAVET_ESHAPE, "gemm16: N or K not a multiple of the tile");

@@ -30,26 +30,16 @@ struct Layout {
   size_t total;
 };
 
-// Bytes of fp32 partial tiles the 16-bit GEMMs of a step may need.  A split
-// is only planned while (tiles * ksplit) < 256 before the last doubling, so
-// tiles * ksplit < 512 and the partials never exceed 512 tiles of 256 x 256.
+// Bytes of fp32 partial tiles the 16-bit GEMMs of a step with at most
+// `tokens` rows may need (the largest over the four projections).
 static size_t partial_bytes(const davet_model_cfg& c, int64_t tokens) {
   if (!is16(c.dtype)) return 0;
   const int64_t Ns[4] = {3LL * c.d, c.d, 2LL * c.ffn, c.d};
   const int64_t Ks[4] = {c.d, c.d, c.d, c.ffn};
   size_t best = 0;
-  for (int g = 0; g < 4; ++g) {
-    // worst case over token counts 1..tokens, sampled where plans change
-    for (int64_t m = 1; m <= tokens; m = m < 64 ? m + 1 : m + (m >> 4)) {
-      const GemmPlan p = plan_gemm16((int)m, (int)Ns[g], (int)Ks[g]);
-      if (p.ksplit > 1)
-        best = std::max(best, (size_t)p.ksplit * m * Ns[g] * 4);
-    }
-    const GemmPlan p = plan_gemm16((int)tokens, (int)Ns[g], (int)Ks[g]);
-    if (p.ksplit > 1)
-      best = std::max(best, (size_t)p.ksplit * tokens * Ns[g] * 4);
-  }
-  return std::min<size_t>(best, (size_t)512 * 256 * 256 * 4);
+  for (int g = 0; g < 4; ++g)
+    best = std::max(best, gemm16_partial_bound((int)tokens, (int)Ns[g], (int)Ks[g]));
+  return best;
 }
 
 static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
@@ -270,6 +260,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   const float* rope = rope_cs ? rope_cs : reinterpret_cast<float*>(ws + lay.rope);
   int32_t* pos = reinterpret_cast<int32_t*>(ws + lay.pos);
   float* part = reinterpret_cast<float*>(ws + lay.part);
+  const size_t part_cap = partial_bytes(c, total);
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
   void* Hm = ws + lay.Hm;
   const int rows = n_seqs * L;
@@ -300,7 +291,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
       // QKV projection, rotary embedding on the query and key columns
       RUN(launch_gemm16(dt, EPI_STORE, p_qkv, Ah, (const uint16_t*)lw.wqkv,
                         nullptr, QKV, T, 3 * d, d, 3 * d, pos, rope, 2 * d,
-                        part, KC_GEMM_QKV, s));
+                        part, part_cap, KC_GEMM_QKV, s));
       if (p_qkv.ksplit > 1)
         RUN(launch_reduce_store_rope(dt, part, p_qkv.ksplit, T, 3 * d, 2 * d,
                                      pos, rope, QKV, s));
@@ -309,7 +300,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
       // X += O Wo^T, then A = RMSNorm(X) for the feed-forward block
       RUN(launch_gemm16(dt, EPI_ADD_F32, p_o, (const uint16_t*)O,
                         (const uint16_t*)lw.wo, nullptr, X, T, d, d, d,
-                        nullptr, nullptr, 0, part, KC_GEMM_O, s));
+                        nullptr, nullptr, 0, part, part_cap, KC_GEMM_O, s));
       if (p_o.ksplit > 1)
         RUN(launch_reduce_add_norm(dt, part, p_o.ksplit, T, d, X, lw.ffn_norm,
                                    c.rms_eps, A, s));
@@ -317,13 +308,13 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
         RUN(launch_rmsnorm(X, T, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
       RUN(launch_gemm16(dt, EPI_SWIGLU, p_gu, Ah, (const uint16_t*)lw.wg,
                         (const uint16_t*)lw.wu, H, T, 2 * F, d, F, nullptr,
-                        nullptr, 0, part, KC_GEMM_GATEUP, s));
+                        nullptr, 0, part, part_cap, KC_GEMM_GATEUP, s));
       if (p_gu.ksplit > 1)
         RUN(launch_reduce_swiglu(dt, part, p_gu.ksplit, T, F, H, s));
       // X += H Wd^T (and the next layer's input norm when reducing splits)
       RUN(launch_gemm16(dt, EPI_ADD_F32, p_dn, (const uint16_t*)H,
                         (const uint16_t*)lw.wd, nullptr, X, T, d, F, d,
-                        nullptr, nullptr, 0, part, KC_GEMM_DOWN, s));
+                        nullptr, nullptr, 0, part, part_cap, KC_GEMM_DOWN, s));
       a_ready = false;
       if (p_dn.ksplit > 1) {
         const bool next = l + 1 < c.n_layers;
