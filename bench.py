@@ -57,6 +57,10 @@ def parse():
     ap.add_argument("--mode", choices=["f16", "bf16"], default="f16",
                     help="16-bit operand format for a bf16 model (f16: its "
                          "weights converted exactly; default)")
+    ap.add_argument("--head-layout", choices=["tiled", "rows"],
+                    default="tiled",
+                    help="vocabulary-head weight layout of a 16-bit model "
+                         "(tiled: davet_pack_head at setup; default)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only stream MIB MiB of fp32 through a plain "
                          "elementwise copy (y = x * 1) five times and exit: "
@@ -80,7 +84,7 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
-def setup(cfg, mode):
+def setup(cfg, mode, head_layout="tiled"):
     import numpy as np
     import torch
 
@@ -111,7 +115,16 @@ def setup(cfg, mode):
         del lw
     embed = dev(synth.gen_embed(cfg, as_bits=bf))
     head = dev(synth.gen_head(cfg, as_bits=bf))
-    W = dv.Weights(embed, head, layers)
+    layout = dv.DAVET_HEAD_ROWS
+    if bf and head_layout == "tiled":
+        # model-load transform: the vocabulary head in the tiled layout the
+        # head kernel streams in order (logits bit-identical to row-major)
+        tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
+                            dtype=torch.int16, device="cuda")
+        dv.davet_pack_head(head, tiled, cfg.vocab, cfg.d, dtype)
+        torch.cuda.synchronize()
+        head, layout = tiled, dv.DAVET_HEAD_TILED
+    W = dv.Weights(embed, head, layers, head_layout=layout)
     s = synth.gen_sample(cfg, as_bits=bf)
     n = cfg.n_seqs
     geoms, visual, view_bufs, sizes = [], [], [], []
@@ -334,7 +347,7 @@ def main():
 
     cfg = synth.get_config(args.config)
     mode = args.mode if cfg.dtype == "bf16" else "f32"
-    st = setup(cfg, mode)
+    st = setup(cfg, mode, args.head_layout)
     dv = st["dv"]
     for _ in range(args.warmup):
         run_loop(cfg, st)
@@ -406,6 +419,7 @@ def main():
                 "encodings, uniform prompt ids)",
         "config": {
             "workload": cfg.name, "model_dtype": cfg.dtype,
+            "head_layout": args.head_layout if cfg.dtype == "bf16" else "rows",
             "operands": {"f16": "fp16 x fp16 -> fp32 matrix cores, bf16 "
                                 "weights converted exactly",
                          "bf16": "bf16 x bf16 -> fp32 matrix cores",

@@ -103,13 +103,21 @@ typedef struct davet_layer_weights {
   const float* ffn_norm;
 } davet_layer_weights;
 
-/* embed [vocab, d] token embedding; head [vocab, d] untied output head;
- * final_norm float32 [d] or NULL; layers: HOST array of n_layers entries. */
+/* Layout of the vocabulary-head weights (davet_weights.head_layout). */
+typedef enum davet_head_layout {
+  DAVET_HEAD_ROWS = 0,   /* [vocab, d] row-major */
+  DAVET_HEAD_TILED = 1   /* 16-bit models only: the output of davet_pack_head */
+} davet_head_layout;
+
+/* embed [vocab, d] token embedding; head: untied output head, [vocab, d]
+ * row-major or tiled (head_layout); final_norm float32 [d] or NULL; layers:
+ * HOST array of n_layers entries. */
 typedef struct davet_weights {
   const void* embed;
   const void* head;
   const float* final_norm;
   const davet_layer_weights* layers;
+  int32_t head_layout;
 } davet_weights;
 
 /* Allocation policy parameters (Sec. 4.2): average budget B, reserve fraction
@@ -160,6 +168,21 @@ int davet_build_views(const davet_view_geom* g, const void* v,
  * dtypes and must not overlap.  Errors: EINVAL (null, overlap), EDTYPE. */
 int davet_convert(const void* src, int32_t src_dtype, void* dst,
                   int32_t dst_dtype, size_t n, hipStream_t stream);
+
+/* Tiled copy of a 16-bit vocabulary head for the head kernel (a one-time
+ * model-load transform; the logits are bit-identical to those of the
+ * row-major head).  The tiled head is a sequence of 128 x 64 tiles, k-chunk
+ * major, so that every vocabulary slab reads chunk c of its rows from one
+ * contiguous region while all slabs stream chunk c at the same time:
+ *   tiled[((c * S + s) * 128 + r) * 64 + j] = head[(128 s + r) * d + 64 c + j]
+ * with S = ceil(vocab / 128) slabs, c < d / 64, r < 128, j < 64; rows past
+ * vocab are zero.  src [vocab, d] and dst [davet_head_tiled_elems(vocab, d)]
+ * are device buffers of dtype (DAVET_BF16 or DAVET_F16) and must not overlap.
+ * Errors: EINVAL (null, overlap), ESHAPE (vocab < 1, d < 64, d % 64 != 0),
+ * EDTYPE. */
+size_t davet_head_tiled_elems(int32_t vocab, int32_t d);
+int davet_pack_head(const void* src, void* dst, int32_t vocab, int32_t d,
+                    int32_t dtype, hipStream_t stream);
 
 /* ------------------------------------------------------------- denoiser -- */
 

@@ -48,7 +48,12 @@ class LayerWeights(C.Structure):
 class WeightsT(C.Structure):
     _fields_ = [("embed", C.c_void_p), ("head", C.c_void_p),
                 ("final_norm", C.c_void_p),
-                ("layers", C.POINTER(LayerWeights))]
+                ("layers", C.POINTER(LayerWeights)),
+                ("head_layout", C.c_int32)]
+
+
+DAVET_HEAD_ROWS = 0
+DAVET_HEAD_TILED = 1
 
 
 class Policy(C.Structure):
@@ -75,6 +80,8 @@ _SIGS = {
     "davet_build_views": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
                                     _P_vp, _vp]),
     "davet_convert": (C.c_int, [_vp, _i32, _vp, _i32, C.c_size_t, _vp]),
+    "davet_head_tiled_elems": (C.c_size_t, [_i32, _i32]),
+    "davet_pack_head": (C.c_int, [_vp, _vp, _i32, _i32, _i32, _vp]),
     "davet_workspace_bytes": (C.c_int, [C.POINTER(ModelCfg), _i32, _i32, _i32,
                                         C.POINTER(C.c_size_t)]),
     "davet_denoise_step": (C.c_int, [C.POINTER(ModelCfg), C.POINTER(WeightsT),
@@ -155,9 +162,12 @@ def _i32_array(vals):
 class Weights:
     """Holds the davet_weights struct and keeps the tensors it points to
     alive.  ``layers`` is a list of dicts with tensors wqkv, wo, wg, wu, wd
-    and optional attn_norm / ffn_norm (float32)."""
+    and optional attn_norm / ffn_norm (float32).  ``head`` is row-major
+    [vocab, d], or the output of davet_pack_head with
+    head_layout=DAVET_HEAD_TILED."""
 
-    def __init__(self, embed, head, layers, final_norm=None):
+    def __init__(self, embed, head, layers, final_norm=None,
+                 head_layout=DAVET_HEAD_ROWS):
         self._keep = [embed, head, final_norm, layers]
         self._layers = (LayerWeights * max(1, len(layers)))()
         for i, lw in enumerate(layers):
@@ -170,7 +180,7 @@ class Weights:
                 else None)
         self.struct = WeightsT(embed.data_ptr(), head.data_ptr(),
                                final_norm.data_ptr() if final_norm is not None
-                               else None, self._layers)
+                               else None, self._layers, int(head_layout))
 
 
 def davet_version():
@@ -197,6 +207,15 @@ def davet_convert(src, src_dtype, dst, dst_dtype, n=None, stream=None):
     n = src.numel() if n is None else n
     _check(_L.davet_convert(_ptr(src), int(src_dtype), _ptr(dst),
                             int(dst_dtype), int(n), _stream(stream)))
+
+
+def davet_head_tiled_elems(vocab, d):
+    return int(_L.davet_head_tiled_elems(int(vocab), int(d)))
+
+
+def davet_pack_head(src, dst, vocab, d, dtype, stream=None):
+    _check(_L.davet_pack_head(_ptr(src), _ptr(dst), int(vocab), int(d),
+                              int(dtype), _stream(stream)))
 
 
 def davet_workspace_bytes(cfg, max_tokens, max_seqs, L):

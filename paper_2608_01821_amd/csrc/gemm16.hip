@@ -75,6 +75,9 @@ struct EpiArgs {
   // K order: N tile nb starts at slab (nb * krot) mod nk and wraps, so that
   // concurrent workgroups stream different DRAM regions (0: in order)
   int krot;
+  // B is a tiled vocabulary head (BN = 128, BK = 64 only): tile (kt, nb) is a
+  // contiguous row-major [128][64] block at (kt * n_tiles_n + nb) * 8192
+  int b_tiled;
 };
 
 __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
@@ -199,8 +202,11 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     } else {
       gn = min(n0 + r, N - 1);
     }
-    b_src[q] = base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
+    b_src[q] = ep.b_tiled
+                   ? B + ((size_t)kt0 * n_ntiles + nb) * BN * BK + (size_t)r * BK + c * 8
+                   : base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
   }
+  const size_t b_kstride = ep.b_tiled ? (size_t)n_ntiles * BN * BK : (size_t)BK;
 
   // A load instructions of this wave holding at least one live row: rows
   // past the last live one are not fetched (their LDS rows feed only output
@@ -220,7 +226,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       if (q < na) dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
 #pragma unroll
     for (int q = 0; q < BI; ++q)
-      dma16(b_src[q] + (size_t)kt * BK, sb + (wave * BI + q) * 1024);
+      dma16(b_src[q] + (size_t)kt * b_kstride, sb + (wave * BI + q) * 1024);
   };
 
   f32x16 acc[TM][TN];
@@ -603,7 +609,8 @@ int head16_slabs(int vocab) { return (vocab + 127) / 128; }
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s, int variant, int krot) {
+                  float* logits_out, hipStream_t s, int variant, int krot,
+                  int tiled) {
   if (variant < 0) variant = 6;
   // K-order rotation per vocabulary slab: helps the weight stream of an
   // isolated head launch on MI355X but not inside the denoising step (the
@@ -621,6 +628,9 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   ep.parg = parg;
   ep.logits_out = logits_out;
   ep.krot = krot;
+  ep.b_tiled = tiled;
+  if (tiled && (variant != 6 || d % 64))
+    return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
   // 128-column slabs (BN = 128) keep n_slabs = ceil(V / 128)
   // One M slot per vocabulary slab: each workgroup loops over the live row
   // tiles, so late steps with few masked rows launch no idle workgroups (idle

@@ -486,6 +486,28 @@ convert_kernel(const typename Src::st* __restrict__ src,
     dst[i] = Dst::store(Src::load(src[i]));
 }
 
+// Tiled vocabulary head: thread q writes the 16 bytes (8 elements) at
+// tiled[8q .. 8q+8): tile (c, s), row r, elements 8u .. 8u+7 of the 64.
+__global__ void __launch_bounds__(256)
+pack_head_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                 int vocab, int d, int n_slabs, size_t n_vec) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < n_vec;
+       q += stride) {
+    const int u = (int)(q & 7);
+    const size_t rq = q >> 3;                   // row of a tile, globally
+    const int r = (int)(rq & 127);
+    const size_t tile = rq >> 7;                // c * n_slabs + s
+    const int sl = (int)(tile % n_slabs);
+    const int c = (int)(tile / n_slabs);
+    const int n = sl * 128 + r;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (n < vocab)
+      v = *reinterpret_cast<const u32x4*>(src + (size_t)n * d + c * 64 + u * 8);
+    *reinterpret_cast<u32x4*>(dst + q * 8) = v;
+  }
+}
+
 template <typename Src>
 int convert_from(const void* src, void* dst, int dst_dtype, size_t n,
                  hipStream_t s) {
@@ -673,7 +695,44 @@ int launch_head_reduce_f32(const float* logits, const int32_t* list,
   return DAVET_OK;
 }
 
+int launch_pack_head(const uint16_t* src, uint16_t* dst, int vocab, int d,
+                     hipStream_t s) {
+  ProfScope ps(KC_MISC, s);
+  const int n_slabs = (vocab + 127) / 128;
+  const size_t n_vec = (size_t)n_slabs * 128 * d / 8;
+  const size_t blocks = std::min<size_t>((n_vec + 255) / 256, 65536);
+  hipLaunchKernelGGL(pack_head_kernel, dim3(blocks), dim3(256), 0, s, src, dst,
+                     vocab, d, n_slabs, n_vec);
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
 }  // namespace davet
+
+extern "C" size_t davet_head_tiled_elems(int32_t vocab, int32_t d) {
+  if (vocab < 1 || d < 1) return 0;
+  return (size_t)((vocab + 127) / 128) * 128 * (size_t)d;
+}
+
+extern "C" int davet_pack_head(const void* src, void* dst, int32_t vocab,
+                               int32_t d, int32_t dtype, hipStream_t stream) {
+  using namespace davet;
+  DAVET_CHECK_ARG(src && dst, DAVET_EINVAL, "davet_pack_head: null pointer");
+  DAVET_CHECK_ARG(is16(dtype), DAVET_EDTYPE,
+                  "davet_pack_head: dtype must be DAVET_BF16 or DAVET_F16");
+  DAVET_CHECK_ARG(vocab >= 1 && d >= 64 && d % 64 == 0, DAVET_ESHAPE,
+                  "davet_pack_head: vocab >= 1, d >= 64 and d % 64 == 0");
+  DAVET_CHECK_ARG(((uintptr_t)src & 15) == 0 && ((uintptr_t)dst & 15) == 0,
+                  DAVET_EINVAL, "davet_pack_head: buffers must be 16-byte aligned");
+  const char* s0 = static_cast<const char*>(src);
+  const char* d0 = static_cast<const char*>(dst);
+  const size_t sb = (size_t)vocab * d * 2;
+  const size_t db = davet_head_tiled_elems(vocab, d) * 2;
+  DAVET_CHECK_ARG(s0 + sb <= d0 || d0 + db <= s0, DAVET_EINVAL,
+                  "davet_pack_head: src and dst overlap");
+  return launch_pack_head(static_cast<const uint16_t*>(src),
+                          static_cast<uint16_t*>(dst), vocab, d, stream);
+}
 
 extern "C" int davet_convert(const void* src, int32_t src_dtype, void* dst,
                              int32_t dst_dtype, size_t n, hipStream_t stream) {

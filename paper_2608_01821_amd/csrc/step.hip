@@ -202,6 +202,11 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       aligned16(w->final_norm),
                   DAVET_EINVAL,
                   "davet_denoise_step: weights must be 16-byte aligned");
+  DAVET_CHECK_ARG(w->head_layout == DAVET_HEAD_ROWS ||
+                      (w->head_layout == DAVET_HEAD_TILED && is16(c.dtype)),
+                  DAVET_EINVAL,
+                  "davet_denoise_step: head_layout must be DAVET_HEAD_ROWS, or "
+                  "DAVET_HEAD_TILED with a 16-bit model");
   DAVET_CHECK_ARG(n_seqs >= 1 && n_seqs <= DAVET_MAX_SEQS, DAVET_ESHAPE,
                   "davet_denoise_step: n_seqs out of range [1, 64]");
   DAVET_CHECK_ARG(L >= 1 && L <= DAVET_MAX_RESP, DAVET_ESHAPE,
@@ -350,7 +355,8 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
     int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);
     RUN(launch_head16(dt, (const uint16_t*)Hm, (const uint16_t*)w->head, list,
                       rows, c.vocab, d, c.mask_id, pmax, psum, parg,
-                      logits_out, s));
+                      logits_out, s, -1, -1,
+                      w->head_layout == DAVET_HEAD_TILED));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {

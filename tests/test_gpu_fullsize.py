@@ -143,3 +143,29 @@ def test_stack32_full_size_low_view():
                                   masked[None])
     check_sampled(cfg, mdl, sample, 0, ids, masked, g_conf[0], g_am[0],
                   g_lg[0], 8, 4)
+
+
+def test_tiled_head_full_size_bit_identical(one_layer):
+    """The tiled vocabulary head (davet_pack_head) gives the very same
+    confidences, argmaxes and logits as the row-major head at full size."""
+    cfg, mdl, sample = one_layer
+    n = dv.davet_head_tiled_elems(cfg.vocab, cfg.d)
+    tiled = torch.empty(n, dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d,
+                       dv.DAVET_F16 if mdl.mode == "f16" else dv.DAVET_BF16)
+    row_w = mdl.weights
+    mdl.weights = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
+                             head_layout=dv.DAVET_HEAD_TILED)
+    try:
+        rng = np.random.default_rng(3)
+        ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab,
+                                   0.7)
+        t_conf, t_am, t_lg = gpu_step(cfg, mdl, [sample], [1], ids[None],
+                                      masked[None])
+    finally:
+        mdl.weights = row_w
+    r_conf, r_am, r_lg = gpu_step(cfg, mdl, [sample], [1], ids[None],
+                                  masked[None])
+    assert np.array_equal(t_am, r_am)
+    assert np.array_equal(t_conf.view(np.uint32), r_conf.view(np.uint32))
+    assert bool(torch.equal(t_lg, r_lg))

@@ -1,0 +1,109 @@
+"""The tiled vocabulary-head layout: the packing kernel against its defining
+index formula (written out in numpy), and a denoising step with the tiled
+head against the row-major one (bit-identical) and against the oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_01821_amd as dv
+import synth
+from gpu_util import (TOL, Model, Sample, compare, model_cfg, oracle_step,
+                      random_state, workspace)
+
+pytestmark = pytest.mark.gpu
+
+
+def _tiled_reference(head, vocab, d):
+    """tiled[((c*S + s)*128 + r)*64 + j] = head[(128 s + r)*d + 64 c + j],
+    zero past the vocabulary."""
+    S = -(-vocab // 128)
+    pad = np.zeros((S * 128, d), head.dtype)
+    pad[:vocab] = head
+    t = pad.reshape(S, 128, d // 64, 64).transpose(2, 0, 1, 3)
+    return np.ascontiguousarray(t).reshape(-1)
+
+
+@pytest.mark.parametrize("vocab,d", [(1000, 256), (128, 64), (1, 128),
+                                     (126464, 4096)])
+def test_pack_head_matches_formula(vocab, d):
+    rng = np.random.default_rng(vocab + d)
+    head = rng.integers(-2 ** 15, 2 ** 15, (vocab, d), dtype=np.int16)
+    src = torch.from_numpy(head).cuda()
+    n = dv.davet_head_tiled_elems(vocab, d)
+    assert n == -(-vocab // 128) * 128 * d
+    dst = torch.full((n,), 77, dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(src, dst, vocab, d, dv.DAVET_F16)
+    torch.cuda.synchronize()
+    exp = _tiled_reference(head, vocab, d)
+    assert np.array_equal(dst.cpu().numpy(), exp)
+
+
+@pytest.mark.parametrize("cid", [11, 12])
+def test_tiled_head_step(cid):
+    cfg = synth.get_any_config(cid)
+    mdl = Model(cfg)
+    s = synth.gen_sample(cfg)
+    n_seqs = min(cfg.n_seqs, 3)
+    samples = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i])
+               for i in range(n_seqs)]
+    tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
+                        dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d, dv.DAVET_F16)
+    w_tiled = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
+                         head_layout=dv.DAVET_HEAD_TILED)
+    rng = np.random.default_rng(cid)
+    st = [random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.6)
+          for _ in samples]
+    ids = np.stack([a for a, _ in st])
+    masked = np.stack([b for _, b in st])
+    levels = [i % cfg.K for i in range(n_seqs)]
+    L = cfg.resp_len
+    prompt = torch.cat([x.dev_prompt for x in samples])
+    cu = np.concatenate([[0], np.cumsum([len(x.prompt) for x in samples])])
+    views_ = [x.dev_levels[lv] for x, lv in zip(samples, levels)]
+    nview = [x.sizes[lv] for x, lv in zip(samples, levels)]
+    total = sum(nview) + int(cu[-1]) + n_seqs * L
+    outs = []
+    for w in (mdl.weights, w_tiled):
+        ws = workspace(cfg, total, n_seqs, L)
+        d_ids = torch.from_numpy(ids.astype(np.int32)).cuda()
+        d_m = torch.from_numpy(masked.astype(np.uint8)).cuda()
+        conf = torch.empty(n_seqs * L, device="cuda")
+        am = torch.empty(n_seqs * L, dtype=torch.int32, device="cuda")
+        lg = torch.full((n_seqs * L, cfg.vocab), 55.0, device="cuda")
+        dv.davet_denoise_step(model_cfg(cfg), w, views_, nview, prompt, cu,
+                              d_ids, d_m, L, conf, am, lg, ws)
+        torch.cuda.synchronize()
+        outs.append((conf.cpu().numpy(), am.cpu().numpy(), lg.cpu().numpy()))
+    (c0, a0, l0), (c1, a1, l1) = outs
+    assert np.array_equal(a0, a1)
+    assert np.array_equal(c0.view(np.uint32), c1.view(np.uint32))
+    assert np.array_equal(l0.view(np.uint32), l1.view(np.uint32))
+    # and the tiled run against the oracle, sequence by sequence
+    for i in range(n_seqs):
+        pos, rl, ra, rc = oracle_step(cfg, mdl, samples[i], levels[i], ids[i],
+                                      masked[i])
+        sl = slice(i * L, (i + 1) * L)
+        compare(cfg, TOL[mdl.mode], masked[i], c1[sl], a1[sl],
+                l1[sl].reshape(L, cfg.vocab), pos, rl, ra, rc)
+
+
+def test_tiled_head_rejected_for_fp32():
+    cfg = synth.get_any_config(13)
+    mdl = Model(cfg)
+    w = dv.Weights(mdl.dev_embed, mdl.dev_head, mdl.dev_layers,
+                   head_layout=dv.DAVET_HEAD_TILED)
+    s = synth.gen_sample(cfg)
+    smp = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0])
+    L = cfg.resp_len
+    ws = workspace(cfg, smp.sizes[-1] + len(smp.prompt) + L, 1, L)
+    d_ids = torch.full((L,), cfg.mask_id, dtype=torch.int32, device="cuda")
+    d_m = torch.ones(L, dtype=torch.uint8, device="cuda")
+    conf = torch.empty(L, device="cuda")
+    am = torch.empty(L, dtype=torch.int32, device="cuda")
+    with pytest.raises(dv.DavetError):
+        dv.davet_denoise_step(model_cfg(cfg), w, [smp.dev_levels[-1]],
+                              [smp.sizes[-1]], smp.dev_prompt,
+                              [0, len(smp.prompt)], d_ids, d_m, L, conf, am,
+                              None, ws)

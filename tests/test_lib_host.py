@@ -126,3 +126,21 @@ def test_argument_validation_without_gpu():
     _expect(-1, dv.davet_policy_step, pol, 5, 4, lo, up, 0.0, 0.0)
     _expect(-1, dv.davet_policy_step, _pol(0.75, 0.2, 1, 1, True, 9), 1, 4,
             lo, up, 0.0, 0.0)
+
+
+def test_head_tiling_host_checks():
+    """Tiled-head size formula and argument checks (no HIP call is made)."""
+    import ctypes as C
+    assert dv.davet_head_tiled_elems(126464, 4096) == 126464 * 4096
+    assert dv.davet_head_tiled_elems(1000, 256) == 1024 * 256
+    assert dv.davet_head_tiled_elems(1, 64) == 128 * 64
+    assert dv.davet_head_tiled_elems(0, 64) == 0
+    lib = dv.raw()
+    a, b = C.c_void_p(1 << 20), C.c_void_p(1 << 30)
+    assert lib.davet_pack_head(None, b, 1000, 256, dv.DAVET_F16, None) == -1
+    assert lib.davet_pack_head(a, b, 1000, 256, dv.DAVET_F32, None) == -3
+    assert lib.davet_pack_head(a, b, 1000, 100, dv.DAVET_F16, None) == -2
+    assert lib.davet_pack_head(a, b, 0, 256, dv.DAVET_BF16, None) == -2
+    # overlapping source and destination
+    assert lib.davet_pack_head(a, C.c_void_p((1 << 20) + 4096), 1000, 256,
+                               dv.DAVET_F16, None) == -1
