@@ -273,6 +273,69 @@ def roofline(cfg, name, cnt, ms, work, loops):
                 launches=cnt, mean_launch_us=round(ms * 1e3 / cnt, 2))
 
 
+def kernel_rooflines(cfg, kern, work):
+    """Every kernel class with a work model, from the untimed profiled pass
+    (one loop): achieved rate and fraction of its roofline."""
+    peak_mm = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {}
+    for name, (cnt, ms) in kern.items():
+        if not cnt or ms <= 0:
+            continue
+        sec = ms / 1e3
+        if name in MATRIX_CLASSES:
+            ach = work[name] / sec / 1e12
+            out[name] = dict(bound="mfma", achieved=round(ach, 1),
+                             unit="TFLOP/s", frac=round(ach / peak_mm, 4))
+        elif name == "head_gemm":
+            ach = work["head_gemm_bytes"] / sec / 1e9
+            out[name] = dict(bound="hbm", achieved=round(ach, 1), unit="GB/s",
+                             frac=round(ach / PEAK_HBM_GBS, 4))
+        elif name == "views":
+            ach = work["views_bytes"] / sec / 1e9
+            out[name] = dict(bound="hbm", achieved=round(ach, 1), unit="GB/s",
+                             frac=round(ach / PEAK_HBM_GBS, 4))
+    return out
+
+
+def per_level_steps(cfg, st, levels, reps=10):
+    """Denoising step time per view level (the loop's own kernels, one
+    davet_denoise_step + davet_unmask on every sequence at that level, all
+    response positions masked), timed with events; untimed by the bench."""
+    import torch
+    dv = st["dv"]
+    n, L, K = cfg.n_seqs, cfg.resp_len, cfg.K
+    out = {}
+    conf = torch.empty(n * L, device="cuda")
+    am = torch.empty(n * L, dtype=torch.int32, device="cuda")
+    for lv in sorted(set(levels)):
+        views, nview = [], []
+        for i in range(n):
+            views.append(st["visual"][i] if lv == K - 1
+                         else st["view_bufs"][i * (K - 1) + lv])
+            nview.append(st["sizes"][i][lv])
+        times = []
+        for r in range(reps + 2):
+            st["ids"].fill_(cfg.mask_id)
+            st["msk"].fill_(1)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dv.davet_denoise_step(st["mcfg"], st["W"], views, nview,
+                                  st["prompt"], st["cu"], st["ids"], st["msk"],
+                                  L, conf, am, None, st["ws"])
+            dv.davet_unmask(n, L, cfg.k, conf, am, st["ids"], st["msk"])
+            e1.record()
+            e1.synchronize()
+            if r >= 2:
+                times.append(e0.elapsed_time(e1))
+        times.sort()
+        ms = times[len(times) // 2]
+        out[str(lv)] = dict(tokens=sum(nview) + st["cu"][-1] + n * L,
+                            ms_per_step=round(ms, 4),
+                            steps_per_s=round(1e3 / ms, 2))
+    return out
+
+
 def cpu_baseline(cfg, st, n_layers_run):
     """The oracle, as it stands, on this host: one step per level the
     schedule uses (all positions masked, first sample), weighted by how
@@ -392,6 +455,9 @@ def main():
     kernels = {k: dict(launches=c, total_ms=round(ms, 3),
                        mean_us=round(ms * 1e3 / c, 2) if c else 0.0)
                for k, (c, ms) in kern.items() if c}
+    k_roof = kernel_rooflines(cfg, kern, work) if kern else {}
+    views_ms = kern.get("views", (0, 0.0))[1] if kern else None
+    levels_probe = per_level_steps(cfg, st, levels)
     cpu = None
     if not args.no_cpu_baseline:
         try:
@@ -439,6 +505,11 @@ def main():
         "tflops_algorithmic": round(flops_loop * loops / elapsed / 1e12, 2),
         "roofline": rl,
         "kernels_untimed_pass": kernels,
+        "kernel_rooflines_untimed_pass": k_roof,
+        "views_vs_loop": None if views_ms is None else dict(
+            views_ms=round(views_ms, 4), loop_ms=round(ms_loop, 3),
+            share=round(views_ms / ms_loop, 6)),
+        "per_level_all_masked": levels_probe,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
