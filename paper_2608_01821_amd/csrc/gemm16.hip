@@ -27,6 +27,7 @@
 //   EPI_PARTIAL  fp32 partial tile of one K split
 
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -174,7 +175,9 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  // wave-uniform values live in scalar registers (branches on them are
+  // scalar, not exec-masked)
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, hh = lane >> 5;
   const bool dual = (EPI == EPI_SWIGLU) || (EPI == EPI_PARTIAL && ep.dual);
@@ -237,47 +240,63 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // 32-row sub-tiles of this wave that hold live rows (wave-uniform)
-  bool live[TM];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) live[i] = m0 + wm * WROWS + i * 32 < m_live;
+  // 32-row sub-tiles of this wave holding live rows: always a prefix, NL of
+  // them.  The K loop is instantiated per NL, so its body has no branch
+  // between the LDS fragment reads and the matrix ops.
+  const int nl = max(0, min(TM, (m_live - m0 - wm * WROWS + 31) / 32));
 
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, s);
 
-  for (int it = 0; it < nk; ++it) {
-    // slab `it` must have landed; later slabs may still be in flight
-    const int ahead = min(STAGES - 2, nk - 1 - it);
-    static_assert((STAGES - 2) * LPT <= 63, "vmcnt range");
-    wait_vmcnt_rt<0, (STAGES - 2) * LPT>(ahead * lpt_live);
-    barrier_nofence();        // slab visible to all waves; slab it-1 retired
-    if (it + STAGES - 1 < nk) issue((it + STAGES - 1) % STAGES, it + STAGES - 1);
-    const char* sa = smem + (it % STAGES) * S_BYTES;
-    const char* sb = sa + A_BYTES;
+  auto k_loop = [&](auto nl_c) {
+    constexpr int NL = decltype(nl_c)::value;
+    for (int it = 0; it < nk; ++it) {
+      // slab `it` must have landed; later slabs may still be in flight
+      const int ahead = min(STAGES - 2, nk - 1 - it);
+      static_assert((STAGES - 2) * LPT <= 63, "vmcnt range");
+      wait_vmcnt_rt<0, (STAGES - 2) * LPT>(ahead * lpt_live);
+      barrier_nofence();        // slab visible to all waves; slab it-1 retired
+      if (it + STAGES - 1 < nk) issue((it + STAGES - 1) % STAGES, it + STAGES - 1);
+      if constexpr (NL > 0) {
+        const char* sa = smem + (it % STAGES) * S_BYTES;
+        const char* sb = sa + A_BYTES;
+        // fragments of K step kk+1 are read from LDS while the matrix ops of
+        // step kk run (two register sets)
+        v8 af[2][NL], bfr[2][TN];
+        auto load_frags = [&](int kk, v8 (&a)[NL], v8 (&b)[TN]) {
+          const int c = kk * 2 + hh;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = kk * 2 + hh;
-      v8 af[TM], bfr[TN];
+          for (int i = 0; i < NL; ++i) {
+            const int r = wm * WROWS + i * 32 + l32;
+            a[i] = *reinterpret_cast<const v8*>(sa + swz<BK>(r, c));
+          }
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        if (!live[i]) continue;
-        const int r = wm * WROWS + i * 32 + l32;
-        af[i] = *reinterpret_cast<const v8*>(sa + swz<BK>(r, c));
-      }
+          for (int j = 0; j < TN; ++j) {
+            const int r = j * 64 + wn * 32 + l32;
+            b[j] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
+          }
+        };
+        load_frags(0, af[0], bfr[0]);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = j * 64 + wn * 32 + l32;
-        bfr[j] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
-      }
+        for (int kk = 0; kk < BK / 16; ++kk) {
+          if (kk + 1 < BK / 16) load_frags(kk + 1, af[(kk + 1) & 1], bfr[(kk + 1) & 1]);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        if (!live[i]) continue;       // sub-tile past the live rows: no work
+          for (int i = 0; i < NL; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = Fmt::mfma32(af[i], bfr[j], acc[i][j]);
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = Fmt::mfma32(af[kk & 1][i], bfr[kk & 1][j], acc[i][j]);
+        }
       }
     }
+  };
+  static_assert(TM <= 4, "live-prefix dispatch covers up to 4 sub-tiles");
+  switch (nl) {
+    case 0: k_loop(std::integral_constant<int, 0>{}); break;
+    case 1: k_loop(std::integral_constant<int, 1>{}); break;
+    case 2: k_loop(std::integral_constant<int, (TM >= 2 ? 2 : TM)>{}); break;
+    case 3: k_loop(std::integral_constant<int, (TM >= 3 ? 3 : TM)>{}); break;
+    default: k_loop(std::integral_constant<int, TM>{}); break;
   }
 
   // ---------------------------------------------------------------- epilogue
