@@ -467,7 +467,8 @@ using V8 = Var<256, 256, 64, 2, 8>;    // 128 KB, deep slabs, large M
 using V9 = Var<128, 256, 64, 2, 8>;    // 96 KB
 using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
 using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
-constexpr int N_VARIANTS = 12;
+using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
+constexpr int N_VARIANTS = 13;
 
 int variant_bn(int tile) {
   switch (tile) {
@@ -483,7 +484,7 @@ int variant_bm(int tile) {
   }
 }
 int variant_bk(int tile) {
-  return (tile == 4 || (tile >= 6 && tile <= 9)) ? 64 : 32;
+  return (tile == 4 || (tile >= 6 && tile <= 9) || tile == 12) ? 64 : 32;
 }
 
 template <typename Fmt, int EPI>
@@ -503,6 +504,7 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
     case 9: LV(V9);
     case 10: LV(V10);
     case 11: LV(V11);
+    case 12: LV(V12);
     default: LV(V0);
   }
 #undef LV
@@ -534,13 +536,13 @@ constexpr int kNB = 7;
 struct TableShape { int N, K; GemmPlan plan[kNB]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4, 0}, {8, 2, 0}, {6, 1, 0}, {8, 1, 0}, {6, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    {12288, 4096, {{8, 4, 0}, {8, 2, 0}, {12, 1, 0}, {8, 1, 0}, {12, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
+    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {12, 1, 0}, {8, 2, 0}, {8, 1, 0}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{6, 1, 0}, {8, 1, 0}, {6, 1, 0}, {6, 1, 0}, {6, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    {24576, 4096, {{8, 2, 0}, {8, 1, 0}, {12, 1, 0}, {12, 1, 0}, {12, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{6, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
+    {4096, 12288, {{12, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
 };
 
 static const TableShape* table_shape(int N, int K) {
@@ -630,7 +632,10 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
                   float* logits_out, hipStream_t s, int variant, int krot,
                   int tiled) {
-  if (variant < 0) variant = 6;
+  // 8 wavefronts on the 128 x 128 tile: the matrix work of a slab is spread
+  // over twice the waves, so it hides behind the other workgroup's stream
+  // (measured on MI355X: 201 -> 187 us at 2 live rows, 214 -> 192 at 64)
+  if (variant < 0) variant = 12;
   // K-order rotation per vocabulary slab: helps the weight stream of an
   // isolated head launch on MI355X but not inside the denoising step (the
   // measured default there is 0, every slab starting at k = 0)
@@ -648,7 +653,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   ep.logits_out = logits_out;
   ep.krot = krot;
   ep.b_tiled = tiled;
-  if (tiled && (variant != 6 || d % 64))
+  if (tiled && ((variant != 6 && variant != 12) || d % 64))
     return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
   // 128-column slabs (BN = 128) keep n_slabs = ceil(V / 128)
   // One M slot per vocabulary slab: each workgroup loops over the live row
@@ -658,6 +663,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   if (dtype == DAVET_F16) {
     switch (variant) {
       case 0: HV(F16, V0);
+      case 12: HV(F16, V12);
       case 10: HV(F16, V10);
       case 11: HV(F16, V11);
       default: HV(F16, V6);
