@@ -468,23 +468,25 @@ using V9 = Var<128, 256, 64, 2, 8>;    // 96 KB
 using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
 using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
-constexpr int N_VARIANTS = 13;
+using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
+using V14 = Var<256, 128, 64, 2, 16>;  // 96 KB, 16 wavefronts
+constexpr int N_VARIANTS = 15;
 
 int variant_bn(int tile) {
   switch (tile) {
-    case 2: case 3: case 8: case 9: return 256;
+    case 2: case 3: case 8: case 9: case 13: return 256;
     default: return 128;
   }
 }
 int variant_bm(int tile) {
   switch (tile) {
-    case 1: case 3: case 7: case 8: return 256;
+    case 1: case 3: case 7: case 8: case 13: case 14: return 256;
     case 5: return 64;
     default: return 128;
   }
 }
 int variant_bk(int tile) {
-  return (tile == 4 || (tile >= 6 && tile <= 9) || tile == 12) ? 64 : 32;
+  return (tile == 4 || (tile >= 6 && tile <= 9) || tile >= 12) ? 64 : 32;
 }
 
 template <typename Fmt, int EPI>
@@ -505,6 +507,8 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
     case 10: LV(V10);
     case 11: LV(V11);
     case 12: LV(V12);
+    case 13: LV(V13);
+    case 14: LV(V14);
     default: LV(V0);
   }
 #undef LV
@@ -536,13 +540,13 @@ constexpr int kNB = 7;
 struct TableShape { int N, K; GemmPlan plan[kNB]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4, 0}, {8, 2, 0}, {12, 1, 0}, {8, 1, 0}, {12, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    {12288, 4096, {{8, 4, 0}, {13, 2, 0}, {12, 1, 0}, {13, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {12, 1, 0}, {8, 2, 0}, {8, 1, 0}}},
+    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {12, 1, 0}, {12, 1, 0}, {13, 1, 0}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2, 0}, {8, 1, 0}, {12, 1, 0}, {12, 1, 0}, {12, 1, 0}, {8, 1, 0}, {8, 1, 0}}},
+    {24576, 4096, {{8, 2, 0}, {13, 1, 0}, {12, 1, 0}, {12, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{12, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {8, 1, 0}}},
+    {4096, 12288, {{12, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {13, 1, 0}}},
 };
 
 static const TableShape* table_shape(int N, int K) {
@@ -552,12 +556,12 @@ static const TableShape* table_shape(int N, int K) {
 }
 
 // Other shapes: 128 x 128 tiles with 128-byte slabs and two workgroups per CU
-// up to ~2-3K rows, 256 x 256 tiles with 8 wavefronts above; narrow-N
+// up to ~2-3K rows, 256 x 256 tiles with 16 wavefronts above; narrow-N
 // products split K until the grid fills the 256 CUs (tiles * ksplit < 512).
 static GemmPlan plan_generic(int M, int N, int K) {
   GemmPlan p{};
   const bool big = M >= (N >= 16384 ? 2048 : 3000);
-  p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 8 : (K % 64 == 0 ? 6 : 0);
+  p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 13 : (K % 64 == 0 ? 6 : 0);
   const int bm = variant_bm(p.tile), bn = variant_bn(p.tile);
   const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int nk = K / variant_bk(p.tile);
