@@ -469,8 +469,7 @@ using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
 using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
 using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
-using V14 = Var<256, 128, 64, 2, 16>;  // 96 KB, 16 wavefronts
-constexpr int N_VARIANTS = 15;
+constexpr int N_VARIANTS = 14;
 
 int variant_bn(int tile) {
   switch (tile) {
@@ -480,13 +479,13 @@ int variant_bn(int tile) {
 }
 int variant_bm(int tile) {
   switch (tile) {
-    case 1: case 3: case 7: case 8: case 13: case 14: return 256;
+    case 1: case 3: case 7: case 8: case 13: return 256;
     case 5: return 64;
     default: return 128;
   }
 }
 int variant_bk(int tile) {
-  return (tile == 4 || (tile >= 6 && tile <= 9) || tile >= 12) ? 64 : 32;
+  return (tile == 4 || (tile >= 6 && tile <= 9) || tile == 12 || tile == 13) ? 64 : 32;
 }
 
 template <typename Fmt, int EPI>
@@ -508,7 +507,6 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
     case 11: LV(V11);
     case 12: LV(V12);
     case 13: LV(V13);
-    case 14: LV(V14);
     default: LV(V0);
   }
 #undef LV
