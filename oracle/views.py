@@ -13,6 +13,14 @@ Index map of a level (CSR): ``offsets[n_l + 1]`` and ``members[C*G*G]``;
 token j of the level is the mean of rows ``members[offsets[j]:offsets[j+1]]``
 of v, listed row-major inside its window.  Member ids are global:
 ``c*G*G + r*G + s``.
+
+Mixed view (Sec. 4.3: the middle view augments the pooled representation
+with a fixed subset of unpooled tokens; K = 3).  The paper does not say which
+tokens; reading used here: with a stride S >= 2, the raw tokens on the
+lattice r = o, o+S, ... and s = o, o+S, ... of every crop, o = S // 2 (one
+token per S x S cell, near its centre).  Per crop the mixed level lists the
+coarse (level 0) tokens, then the lattice tokens row-major; each lattice
+token is a one-member "window", i.e. the raw token itself.
 """
 
 import numpy as np
@@ -79,13 +87,67 @@ def pool_level(v: np.ndarray, n_crops: int, grid: int, K: int, level: int,
     return out.astype(np.float32)
 
 
+def lattice(grid: int, stride: int):
+    """Row and column indices of the mixed view's raw tokens in one crop."""
+    if stride < 2:
+        raise ValueError("mixed stride must be >= 2")
+    return list(range(stride // 2, grid, stride))
+
+
+def mixed_index_map(n_crops: int, grid: int, stride: int):
+    """CSR map of the mixed level: per crop the coarse windows (side 4), then
+    the lattice tokens as single members."""
+    coarse_offs, coarse_mem = index_map(1, grid, 3, 0)
+    lat = lattice(grid, stride)
+    offsets = [0]
+    members = []
+    for c in range(n_crops):
+        base = c * grid * grid
+        for t in range(len(coarse_offs) - 1):
+            for m in coarse_mem[coarse_offs[t]:coarse_offs[t + 1]]:
+                members.append(base + int(m))
+            offsets.append(len(members))
+        for r in lat:
+            for q in lat:
+                members.append(base + r * grid + q)
+                offsets.append(len(members))
+    return np.asarray(offsets, dtype=np.int32), np.asarray(members, np.int32)
+
+
+def mixed_level(v: np.ndarray, n_crops: int, grid: int, stride: int,
+                out_dtype: str = "f32") -> np.ndarray:
+    """Mixed level: every token is the float64 mean of its members rounded
+    once (a single raw member is returned unchanged)."""
+    offs, mem = mixed_index_map(n_crops, grid, stride)
+    v64 = np.asarray(v, dtype=np.float64)
+    out = np.empty((len(offs) - 1, v.shape[1]), dtype=np.float64)
+    for t in range(len(offs) - 1):
+        acc = np.zeros(v.shape[1], dtype=np.float64)
+        for m in mem[offs[t]:offs[t + 1]]:
+            acc = acc + v64[m]
+        out[t] = acc / float(offs[t + 1] - offs[t])
+    if out_dtype == "bf16":
+        return _round_f64_to_bf16(out)
+    if out_dtype == "f16":
+        return out.astype(np.float16).astype(np.float32)
+    return out.astype(np.float32)
+
+
 def build_views(v: np.ndarray, n_crops: int, grid: int, K: int = 3,
-                out_dtype: str = "f32"):
-    """All K levels (level K-1 is v itself) and their index maps."""
+                out_dtype: str = "f32", mixed_stride: int = 0):
+    """All K levels (level K-1 is v itself) and their index maps; with
+    ``mixed_stride`` (K = 3 only) the middle level is the mixed view."""
     if v.shape[0] != n_crops * grid * grid:
         raise ValueError("v rows != n_crops * grid * grid")
+    if mixed_stride and K != 3:
+        raise ValueError("the mixed view needs K = 3")
     levels, maps = [], []
     for lv in range(K):
+        if mixed_stride and lv == 1:
+            maps.append(mixed_index_map(n_crops, grid, mixed_stride))
+            levels.append(mixed_level(v, n_crops, grid, mixed_stride,
+                                      out_dtype))
+            continue
         maps.append(index_map(n_crops, grid, K, lv))
         if lv == K - 1:
             levels.append(v)

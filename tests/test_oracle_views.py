@@ -151,3 +151,49 @@ def test_f16_single_rounding_from_double():
     got = views.pool_level(xs.reshape(-1, 1), len(xs), 1, 1, 0, "f16")[:, 0]
     exp = np.array([_nearest_f16(float(x)) for x in xs], dtype=np.float32)
     np.testing.assert_array_equal(got, exp)
+
+
+@pytest.mark.parametrize("C,G,S", [(1, 27, 2), (2, 27, 3), (1, 12, 4),
+                                   (3, 5, 2), (1, 1, 2), (2, 7, 5)])
+def test_mixed_view(C, G, S):
+    """Mixed view (Sec. 4.3): the coarse tokens of each crop, unchanged, then
+    the raw lattice tokens bit-for-bit; the map lists exactly those members."""
+    rng = np.random.default_rng(G * 10 + S)
+    d = 8
+    v = rng.standard_normal((C * G * G, d)).astype(np.float32)
+    levels, maps = views.build_views(v, C, G, 3, "f32", mixed_stride=S)
+    coarse = levels[0]
+    n0 = (-(-G // 4)) ** 2
+    lat = [(r, q) for r in range(S // 2, G, S) for q in range(S // 2, G, S)]
+    # lattice from its definition with numpy index arithmetic
+    rr, qq = np.meshgrid(np.arange(G), np.arange(G), indexing="ij")
+    on = ((rr % S) == S // 2) & ((qq % S) == S // 2)
+    assert sorted(zip(rr[on].tolist(), qq[on].tolist())) == lat
+    mix = levels[1]
+    assert mix.shape[0] == C * (n0 + len(lat))
+    offs, mem = maps[1]
+    assert offs[-1] == C * (G * G + len(lat)) == len(mem)
+    per = n0 + len(lat)
+    for c in range(C):
+        blk = mix[c * per:(c + 1) * per]
+        np.testing.assert_array_equal(blk[:n0], coarse[c * n0:(c + 1) * n0])
+        raw = np.asarray([v[c * G * G + r * G + q] for r, q in lat],
+                         np.float32).reshape(-1, d)
+        np.testing.assert_array_equal(blk[n0:], raw)
+        # pooled part of the map covers the crop once; singletons are the
+        # lattice tokens in row-major order
+        t0 = c * per
+        pooled = mem[offs[t0]:offs[t0 + n0]]
+        assert sorted(pooled.tolist()) == list(range(c * G * G,
+                                                     (c + 1) * G * G))
+        singles = [mem[offs[t0 + n0 + k]:offs[t0 + n0 + k + 1]].tolist()
+                   for k in range(len(lat))]
+        assert singles == [[c * G * G + r * G + q] for r, q in lat]
+
+
+def test_mixed_view_needs_three_levels():
+    v = np.zeros((16, 8), np.float32)
+    with pytest.raises(ValueError):
+        views.build_views(v, 1, 4, 4, "f32", mixed_stride=2)
+    with pytest.raises(ValueError):
+        views.build_views(v, 1, 4, 3, "f32", mixed_stride=1)
