@@ -61,6 +61,10 @@ def parse():
                     default="tiled",
                     help="vocabulary-head weight layout of a 16-bit model "
                          "(tiled: davet_pack_head at setup; default)")
+    ap.add_argument("--mixed-stride", type=int, default=0, metavar="S",
+                    help="middle level = the mixed view (coarse tokens plus "
+                         "the raw-token lattice of stride S) instead of the "
+                         "middle pooling level")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only stream MIB MiB of fp32 through a plain "
                          "elementwise copy (y = x * 1) five times and exit: "
@@ -84,7 +88,7 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
-def setup(cfg, mode, head_layout="tiled"):
+def setup(cfg, mode, head_layout="tiled", mixed_stride=0):
     import numpy as np
     import torch
 
@@ -130,7 +134,8 @@ def setup(cfg, mode, head_layout="tiled"):
     geoms, visual, view_bufs, sizes = [], [], [], []
     tdt = torch.int16 if bf else torch.float32
     for i in range(n):
-        g = dv.ViewGeom(s["n_crops"][i], cfg.grid, cfg.d, cfg.K, dtype)
+        g = dv.ViewGeom(s["n_crops"][i], cfg.grid, cfg.d, cfg.K, dtype,
+                        mixed_stride)
         sz = dv.davet_view_sizes(g)
         geoms.append(g)
         sizes.append(sz)
@@ -298,7 +303,7 @@ def kernel_rooflines(cfg, kern, work):
 
 
 def per_level_steps(cfg, st, levels, reps=10):
-    """Denoising step time per view level (the loop's own kernels, one
+    """Denoising step time at every view level (the loop's own kernels, one
     davet_denoise_step + davet_unmask on every sequence at that level, all
     response positions masked), timed with events; untimed by the bench."""
     import torch
@@ -307,7 +312,7 @@ def per_level_steps(cfg, st, levels, reps=10):
     out = {}
     conf = torch.empty(n * L, device="cuda")
     am = torch.empty(n * L, dtype=torch.int32, device="cuda")
-    for lv in sorted(set(levels)):
+    for lv in range(K):
         views, nview = [], []
         for i in range(n):
             views.append(st["visual"][i] if lv == K - 1
@@ -410,7 +415,7 @@ def main():
 
     cfg = synth.get_config(args.config)
     mode = args.mode if cfg.dtype == "bf16" else "f32"
-    st = setup(cfg, mode, args.head_layout)
+    st = setup(cfg, mode, args.head_layout, args.mixed_stride)
     dv = st["dv"]
     for _ in range(args.warmup):
         run_loop(cfg, st)
@@ -486,6 +491,8 @@ def main():
         "config": {
             "workload": cfg.name, "model_dtype": cfg.dtype,
             "head_layout": args.head_layout if cfg.dtype == "bf16" else "rows",
+            "middle_view": ("mixed, lattice stride %d" % args.mixed_stride
+                            if args.mixed_stride else "pooled (2x2 windows)"),
             "operands": {"f16": "fp16 x fp16 -> fp32 matrix cores, bf16 "
                                 "weights converted exactly",
                          "bf16": "bf16 x bf16 -> fp32 matrix cores",

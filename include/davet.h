@@ -63,13 +63,16 @@ typedef enum davet_dtype { DAVET_F32 = 0, DAVET_BF16 = 1, DAVET_F16 = 2 } davet_
 
 /* Geometry of one sample's visual encoding v: n_crops crops of grid x grid
  * tokens, each token a d-vector; v is [n_crops*grid*grid, d], crop-major, then
- * row-major inside a crop.  K ordered levels, level K-1 being v itself. */
+ * row-major inside a crop.  K ordered levels, level K-1 being v itself.
+ * mixed_stride: 0 for the pooling pyramid; S >= 2 (K = 3 only) makes level 1
+ * the mixed view of Sec. 4.3 (see davet_build_views). */
 typedef struct davet_view_geom {
   int32_t n_crops;
   int32_t grid;
   int32_t d;
   int32_t K;          /* 1..DAVET_MAX_LEVELS */
   int32_t dtype;      /* davet_dtype of v and of the pooled levels */
+  int32_t mixed_stride;
 } davet_view_geom;
 
 /* Denoiser shape.  d = n_heads * head_dim, head_dim in {64, 128} (128 in the
@@ -139,8 +142,16 @@ const char* davet_version(void);
 
 /* Token counts of the K levels of a geometry (host out[K]).  Level l pools
  * windows of side 2^(K-1-l) per crop with ceil padding:
- * n_l = n_crops * ceil(grid / 2^(K-1-l))^2. */
+ * n_l = n_crops * ceil(grid / 2^(K-1-l))^2; the mixed level has
+ * n_1 = n_crops * (ceil(grid / 4)^2 + m^2), m = #{o, o+S, ... < grid},
+ * o = S / 2.  Errors: EINVAL, ESHAPE (bad K, grid, n_crops or stride). */
 int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens /*host[K]*/);
+
+/* Lengths of the K member lists of davet_build_views' index maps (host
+ * out[K]): n_crops * grid^2 per pyramid level, n_crops * (grid^2 + m^2) for
+ * the mixed level. */
+int davet_view_map_sizes(const davet_view_geom* g,
+                         int32_t* n_members /*host[K]*/);
 
 /* Evidence hierarchy (Sec. 4.3, "Ordered evidence hierarchy"; Sec. 3.2: a full
  * budget leaves v unchanged).  Level l < K-1 token j is the mean of the
@@ -151,13 +162,18 @@ int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens /*host[K]*/);
  *   levels       HOST array of K device pointers; levels[l] receives
  *                [n_l, d] for l < K-1; levels[K-1] is ignored (may be NULL)
  *   idx_offsets  HOST array of K device pointers (int32 [n_l + 1]) or NULL;
- *   idx_members  HOST array of K device pointers (int32 [n_crops*grid*grid])
- *                or NULL.  CSR map: token j of level l pools rows
+ *   idx_members  HOST array of K device pointers (int32 [davet_view_map_sizes
+ *                entry]) or NULL.  CSR map: token j of level l pools rows
  *                members[offsets[j] .. offsets[j+1]) of v, listed row-major in
  *                the window, ids c*grid*grid + r*grid + s.  Individual entries
  *                may be NULL to skip that level's map.
+ * Mixed view (mixed_stride = S >= 2, K = 3; Sec. 4.3: the pooled view
+ * augmented with a fixed subset of unpooled tokens): per crop, the level-0
+ * tokens (windows of side 4) followed by the raw tokens at rows and columns
+ * o, o+S, o+2S, ... (o = S/2), row-major, each a one-member window copied
+ * bit for bit from v.
  * Errors: EINVAL (null v / levels entry), ESHAPE (grid<1, n_crops<1, K out of
- * range, d % 8 != 0), EDTYPE. */
+ * range, d % 8 != 0, mixed_stride 1 or < 0, or > 0 with K != 3), EDTYPE. */
 int davet_build_views(const davet_view_geom* g, const void* v,
                       void* const* levels, int32_t* const* idx_offsets,
                       int32_t* const* idx_members, hipStream_t stream);

@@ -11,6 +11,7 @@ from ._lib import (  # noqa: F401
     davet_build_views, davet_convert, davet_demand_prior, davet_denoise_step,
     davet_head_tiled_elems, davet_pack_head,
     davet_policy_envelope, davet_policy_step, davet_run_schedule,
-    davet_step_stats, davet_unmask, davet_version, davet_view_sizes,
+    davet_step_stats, davet_unmask, davet_version, davet_view_map_sizes,
+    davet_view_sizes,
     davet_workspace_bytes, prof_enable, prof_only, prof_read, prof_reset, raw,
 )

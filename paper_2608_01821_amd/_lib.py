@@ -28,7 +28,8 @@ class DavetError(RuntimeError):
 
 class ViewGeom(C.Structure):
     _fields_ = [("n_crops", C.c_int32), ("grid", C.c_int32), ("d", C.c_int32),
-                ("K", C.c_int32), ("dtype", C.c_int32)]
+                ("K", C.c_int32), ("dtype", C.c_int32),
+                ("mixed_stride", C.c_int32)]
 
 
 class ModelCfg(C.Structure):
@@ -77,6 +78,7 @@ _SIGS = {
     "davet_last_error": (C.c_char_p, []),
     "davet_version": (C.c_char_p, []),
     "davet_view_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
+    "davet_view_map_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
     "davet_build_views": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
                                     _P_vp, _vp]),
     "davet_convert": (C.c_int, [_vp, _i32, _vp, _i32, C.c_size_t, _vp]),
@@ -190,6 +192,12 @@ def davet_version():
 def davet_view_sizes(geom: ViewGeom):
     out = (C.c_int32 * geom.K)()
     _check(_L.davet_view_sizes(C.byref(geom), out))
+    return list(out)
+
+
+def davet_view_map_sizes(geom: ViewGeom):
+    out = (C.c_int32 * geom.K)()
+    _check(_L.davet_view_map_sizes(C.byref(geom), out))
     return list(out)
 
 

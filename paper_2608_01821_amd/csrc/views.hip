@@ -5,6 +5,11 @@
 // float64 sum of the sub-window it belongs to at every finer level.  Each
 // level token is then (sum / member count) rounded once to the view dtype.
 // HBM-bound: v is read once, the levels are written once.
+//
+// Mixed view (K = 3, stride S): level 1 becomes, per crop, the level-0 tokens
+// followed by the raw tokens on the lattice (o + aS, o + bS), o = S/2.  The
+// same pass writes each level-0 token twice and copies each lattice token's
+// bits from v; the 2x2 sums are not formed.
 
 #include "common.h"
 
@@ -14,10 +19,17 @@ namespace {
 struct LevelOut { void* p[DAVET_MAX_LEVELS]; };
 
 
-template <int K, int VEC, typename Fmt>
+// lattice length of a crop: #{o, o + S, ... < G}, o = S / 2
+__host__ __device__ inline int lattice_len(int G, int S) {
+  const int o = S / 2;
+  return o < G ? (G - o + S - 1) / S : 0;
+}
+
+template <int K, int VEC, typename Fmt, bool MIXED>
 __global__ void __launch_bounds__(256)
 pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
-                  int n_crops, int G, int d) {
+                  int n_crops, int G, int d, int S) {
+  static_assert(!MIXED || K == 3, "the mixed view is defined for K = 3");
   using T = typename Fmt::st;
   constexpr int F = 1 << (K - 1);                 // coarsest window side
   const int Wc = (G + F - 1) / F;
@@ -66,9 +78,20 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
           x[e] = w.x; x[e + 1] = w.y;
         }
       }
+      if constexpr (MIXED) {
+        const int o = S / 2;
+        if (r % S == o && s % S == o) {           // lattice token: copy bits
+          const int m = lattice_len(G, S);
+          const size_t tok = (size_t)c * (Wc * Wc + m * m) + Wc * Wc +
+                             (size_t)(r / S) * m + (s / S);
+          T* dst = reinterpret_cast<T*>(out.p[1]) + tok * d + e0;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) dst[e] = src[e];
+        }
+      }
       int base = 0;
 #pragma unroll
-      for (int l = 0; l < K - 1; ++l) {
+      for (int l = 0; l < (MIXED ? 1 : K - 1); ++l) {
         const int f = F >> l;                      // window side of level l
         const int per = F / f;                     // sub-windows per side
         const int a = base + (dr / f) * per + (ds / f);
@@ -80,7 +103,7 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
   }
   int base = 0;
 #pragma unroll
-  for (int l = 0; l < K - 1; ++l) {
+  for (int l = 0; l < (MIXED ? 1 : K - 1); ++l) {
     const int f = F >> l;
     const int per = F / f;
     const int W = (G + f - 1) / f;
@@ -97,6 +120,12 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
         const double cnt = (double)(rows * cols);
         const size_t tok = (size_t)c * W * W + (size_t)i * W + j;
         double* ac = acc[base + a * per + b];
+        // level-0 tokens of the mixed view sit at the head of their crop
+        size_t tok_mix = 0;
+        if constexpr (MIXED) {
+          const int m = lattice_len(G, S);
+          tok_mix = (size_t)c * (W * W + m * m) + (size_t)i * W + j;
+        }
         if constexpr (sizeof(T) == 2) {
           uint16_t* dst = reinterpret_cast<uint16_t*>(out.p[l]) + tok * d + e0;
           uint16_t h[VEC];
@@ -108,9 +137,15 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
             for (int q = 0; q < 4; ++q)
               w[q] = (uint32_t)h[2 * q] | ((uint32_t)h[2 * q + 1] << 16);
             *reinterpret_cast<u32x4*>(dst) = w;
+            if constexpr (MIXED)
+              *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out.p[1]) +
+                                        tok_mix * d + e0) = w;
           } else {
-            *reinterpret_cast<uint32_t*>(dst) =
-                (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+            const uint32_t w = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+            *reinterpret_cast<uint32_t*>(dst) = w;
+            if constexpr (MIXED)
+              *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(out.p[1]) +
+                                           tok_mix * d + e0) = w;
           }
         } else {
           float* dst = reinterpret_cast<float*>(out.p[l]) + tok * d + e0;
@@ -120,6 +155,9 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
             w.x = (float)(ac[e] / cnt);
             w.y = (float)(ac[e + 1] / cnt);
             *reinterpret_cast<float2*>(dst + e) = w;
+            if constexpr (MIXED)
+              *reinterpret_cast<float2*>(reinterpret_cast<float*>(out.p[1]) +
+                                         tok_mix * d + e0 + e) = w;
           }
         }
       }
@@ -132,38 +170,51 @@ struct MapOut { int32_t* offs[DAVET_MAX_LEVELS]; int32_t* mem[DAVET_MAX_LEVELS];
 
 // One thread per token of v; for every level it writes the token's slot in
 // that level's member list and, for a window's first token, the window offset.
+// The mixed level (S > 0, level 1) repeats level 0's lists crop by crop
+// (crop stride G^2 + m^2 members, W^2 + m^2 tokens) and appends each lattice
+// token as a one-member window.
 __global__ void __launch_bounds__(256)
-view_maps_kernel(MapOut mo, int n_crops, int G, int K) {
+view_maps_kernel(MapOut mo, int n_crops, int G, int K, int S) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   const int total = n_crops * G * G;
   if (p >= total) return;
   const int c = p / (G * G);
   const int r = (p / G) % G;
   const int s = p % G;
+  const int m = S > 0 ? lattice_len(G, S) : 0;
   for (int l = 0; l < K; ++l) {
-    const int f = 1 << (K - 1 - l);
+    const bool mixed = S > 0 && l == 1;
+    const int f = 1 << (K - 1 - (mixed ? 0 : l));
     const int W = (G + f - 1) / f;
     const int i = r / f, j = s / f;
     const int rows = min(f, G - i * f), cols = min(f, G - j * f);
-    const int off = c * G * G + i * f * G + rows * j * f;
+    const int mem_crop = mixed ? G * G + m * m : G * G;   // members per crop
+    const int tok_crop = mixed ? W * W + m * m : W * W;   // tokens per crop
+    const int off = c * mem_crop + i * f * G + rows * j * f;
     const int a = r - i * f, b = s - j * f;
     if (mo.mem[l]) mo.mem[l][off + a * cols + b] = p;
     if (mo.offs[l]) {
-      if (a == 0 && b == 0) mo.offs[l][c * W * W + i * W + j] = off;
-      if (p == 0) mo.offs[l][n_crops * W * W] = total;
+      if (a == 0 && b == 0) mo.offs[l][c * tok_crop + i * W + j] = off;
+      if (p == 0) mo.offs[l][n_crops * tok_crop] = n_crops * mem_crop;
+    }
+    if (mixed && r % S == S / 2 && s % S == S / 2) {
+      const int k = (r / S) * m + (s / S);
+      const int slot = c * mem_crop + G * G + k;
+      if (mo.mem[l]) mo.mem[l][slot] = p;
+      if (mo.offs[l]) mo.offs[l][c * tok_crop + W * W + k] = slot;
     }
   }
 }
 
-template <int K, int VEC, typename Fmt>
+template <int K, int VEC, typename Fmt, bool MIXED = false>
 void launch_pool(const davet_view_geom& g, const void* v, const LevelOut& lo,
                  hipStream_t s) {
   constexpr int F = 1 << (K - 1);
   const int Wc = (g.grid + F - 1) / F;
   dim3 grid(g.n_crops * Wc * Wc, (g.d / VEC + 255) / 256);
-  hipLaunchKernelGGL((pool_views_kernel<K, VEC, Fmt>), grid, dim3(256), 0, s,
-                     reinterpret_cast<const typename Fmt::st*>(v), lo,
-                     g.n_crops, g.grid, g.d);
+  hipLaunchKernelGGL((pool_views_kernel<K, VEC, Fmt, MIXED>), grid, dim3(256),
+                     0, s, reinterpret_cast<const typename Fmt::st*>(v), lo,
+                     g.n_crops, g.grid, g.d, g.mixed_stride);
 }
 
 template <typename Fmt>
@@ -171,7 +222,10 @@ void launch_pool_k(const davet_view_geom& g, const void* v, const LevelOut& lo,
                    hipStream_t s) {
   switch (g.K) {
     case 2: launch_pool<2, 8, Fmt>(g, v, lo, s); break;
-    case 3: launch_pool<3, 8, Fmt>(g, v, lo, s); break;
+    case 3:
+      if (g.mixed_stride > 0) launch_pool<3, 8, Fmt, true>(g, v, lo, s);
+      else launch_pool<3, 8, Fmt>(g, v, lo, s);
+      break;
     default: launch_pool<4, 2, Fmt>(g, v, lo, s); break;
   }
 }
@@ -204,24 +258,57 @@ int launch_view_maps(const davet_view_geom& g, int32_t* const* offs,
   const int total = g.n_crops * g.grid * g.grid;
   ProfScope ps(KC_VIEW_MAPS, s);
   hipLaunchKernelGGL(view_maps_kernel, dim3((total + 255) / 256), dim3(256), 0,
-                     s, mo, g.n_crops, g.grid, g.K);
+                     s, mo, g.n_crops, g.grid, g.K, g.mixed_stride);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
 
 }  // namespace davet
 
+namespace davet {
+static int check_geom(const davet_view_geom* g, const char* who) {
+  DAVET_CHECK_ARG(g->K >= 1 && g->K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
+                  std::string(who) + ": K out of range [1, 4]");
+  DAVET_CHECK_ARG(g->grid >= 1 && g->n_crops >= 1, DAVET_ESHAPE,
+                  std::string(who) + ": grid and n_crops must be >= 1");
+  DAVET_CHECK_ARG(g->mixed_stride == 0 || (g->mixed_stride >= 2 && g->K == 3),
+                  DAVET_ESHAPE,
+                  std::string(who) + ": mixed_stride must be 0, or >= 2 with K = 3");
+  DAVET_CHECK_ARG((long long)g->n_crops * g->grid * g->grid * 2 < (1ll << 31),
+                  DAVET_ESHAPE, std::string(who) + ": too many tokens");
+  return DAVET_OK;
+}
+}  // namespace davet
+
 extern "C" int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens) {
   using namespace davet;
   DAVET_CHECK_ARG(g && n_tokens, DAVET_EINVAL, "davet_view_sizes: null argument");
-  DAVET_CHECK_ARG(g->K >= 1 && g->K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
-                  "davet_view_sizes: K out of range");
-  DAVET_CHECK_ARG(g->grid >= 1 && g->n_crops >= 1, DAVET_ESHAPE,
-                  "davet_view_sizes: grid and n_crops must be >= 1");
+  int rc = check_geom(g, "davet_view_sizes");
+  if (rc) return rc;
   for (int l = 0; l < g->K; ++l) {
     const int f = 1 << (g->K - 1 - l);
     const int W = (g->grid + f - 1) / f;
     n_tokens[l] = g->n_crops * W * W;
+  }
+  if (g->mixed_stride > 0) {
+    const int W0 = (g->grid + 3) / 4;
+    const int m = lattice_len(g->grid, g->mixed_stride);
+    n_tokens[1] = g->n_crops * (W0 * W0 + m * m);
+  }
+  return DAVET_OK;
+}
+
+extern "C" int davet_view_map_sizes(const davet_view_geom* g,
+                                    int32_t* n_members) {
+  using namespace davet;
+  DAVET_CHECK_ARG(g && n_members, DAVET_EINVAL,
+                  "davet_view_map_sizes: null argument");
+  int rc = check_geom(g, "davet_view_map_sizes");
+  if (rc) return rc;
+  for (int l = 0; l < g->K; ++l) n_members[l] = g->n_crops * g->grid * g->grid;
+  if (g->mixed_stride > 0) {
+    const int m = lattice_len(g->grid, g->mixed_stride);
+    n_members[1] = g->n_crops * (g->grid * g->grid + m * m);
   }
   return DAVET_OK;
 }
@@ -233,17 +320,15 @@ extern "C" int davet_build_views(const davet_view_geom* g, const void* v,
                                  hipStream_t stream) {
   using namespace davet;
   DAVET_CHECK_ARG(g && v, DAVET_EINVAL, "davet_build_views: null geometry or v");
-  DAVET_CHECK_ARG(g->K >= 1 && g->K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
-                  "davet_build_views: K out of range [1, 4]");
-  DAVET_CHECK_ARG(g->grid >= 1 && g->n_crops >= 1, DAVET_ESHAPE,
-                  "davet_build_views: grid and n_crops must be >= 1");
+  {
+    int rc = check_geom(g, "davet_build_views");
+    if (rc) return rc;
+  }
   DAVET_CHECK_ARG(g->d >= 8 && g->d % 8 == 0, DAVET_ESHAPE,
                   "davet_build_views: d must be a positive multiple of 8");
   DAVET_CHECK_ARG(g->dtype == DAVET_F32 || g->dtype == DAVET_BF16 ||
                       g->dtype == DAVET_F16, DAVET_EDTYPE,
                   "davet_build_views: dtype must be DAVET_F32, BF16 or F16");
-  DAVET_CHECK_ARG((long long)g->n_crops * g->grid * g->grid < (1ll << 31),
-                  DAVET_ESHAPE, "davet_build_views: too many tokens");
   if (g->K > 1) {
     DAVET_CHECK_ARG(levels != nullptr, DAVET_EINVAL,
                     "davet_build_views: levels is null");

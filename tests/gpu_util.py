@@ -60,9 +60,10 @@ def model_cfg(cfg, mode=None):
                        DTYPE[mode])
 
 
-def view_geom(cfg, n_crops, mode=None):
+def view_geom(cfg, n_crops, mode=None, mixed_stride=0):
     mode = mode or default_mode(cfg)
-    return dv.ViewGeom(n_crops, cfg.grid, cfg.d, cfg.K, DTYPE[mode])
+    return dv.ViewGeom(n_crops, cfg.grid, cfg.d, cfg.K, DTYPE[mode],
+                       mixed_stride)
 
 
 class Model:
@@ -105,7 +106,8 @@ class Model:
 class Sample:
     """One sample's inputs on both sides and its GPU-built views."""
 
-    def __init__(self, cfg, n_crops, visual, prompt, mode=None):
+    def __init__(self, cfg, n_crops, visual, prompt, mode=None,
+                 mixed_stride=0):
         self.cfg = cfg
         self.mode = mode = mode or default_mode(cfg)
         dev_v, host_v = to_mode(visual, mode)
@@ -113,8 +115,8 @@ class Sample:
         self.prompt = prompt
         self.n_crops = n_crops
         self.ref_levels, _ = views.build_views(host_v, n_crops, cfg.grid,
-                                               cfg.K, mode)
-        geom = view_geom(cfg, n_crops, mode)
+                                               cfg.K, mode, mixed_stride)
+        geom = view_geom(cfg, n_crops, mode, mixed_stride)
         self.sizes = dv.davet_view_sizes(geom)
         self.dev_v = torch.from_numpy(dev_v).cuda()
         tdt = torch.float32 if mode == "f32" else torch.int16

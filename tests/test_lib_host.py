@@ -144,3 +144,22 @@ def test_head_tiling_host_checks():
     # overlapping source and destination
     assert lib.davet_pack_head(a, C.c_void_p((1 << 20) + 4096), 1000, 256,
                                dv.DAVET_F16, None) == -1
+
+
+def test_mixed_view_sizes_host():
+    """Mixed-view token and member counts (Sec. 4.3 reading: coarse tokens
+    plus the raw lattice o, o+S, ..., o = S/2), and geometry checks."""
+    for C, G, S in [(1, 27, 2), (5, 27, 3), (2, 12, 4), (1, 1, 2), (3, 7, 5)]:
+        lat = len(range(S // 2, G, S))
+        g = dv.ViewGeom(C, G, 64, 3, dv.DAVET_BF16, S)
+        n0 = -(-G // 4)
+        n1 = -(-G // 2)
+        assert dv.davet_view_sizes(g) == [C * n0 * n0, C * (n0 * n0 + lat * lat),
+                                          C * G * G]
+        assert dv.davet_view_map_sizes(g) == [C * G * G,
+                                              C * (G * G + lat * lat), C * G * G]
+        g0 = dv.ViewGeom(C, G, 64, 3, dv.DAVET_BF16)
+        assert dv.davet_view_sizes(g0)[1] == C * n1 * n1
+    for bad in (dv.ViewGeom(1, 27, 64, 4, 1, 2), dv.ViewGeom(1, 27, 64, 3, 1, 1),
+                dv.ViewGeom(1, 27, 64, 3, 1, -2)):
+        _expect(-2, dv.davet_view_sizes, bad)
