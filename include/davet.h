@@ -262,6 +262,18 @@ int davet_unmask(int32_t n_seqs, int32_t L, int32_t k, const float* conf,
  * unknown category. */
 double davet_demand_prior(int32_t category);
 
+/* Operation parser g (App. A, "Operation Parser and Demand Prior"): the
+ * category of a query text (NUL-terminated, any case), host only.  The
+ * query is lowercased, generic conversation wrappers ("<image>", "answer
+ * the question using a single word or phrase", "in the image", ...) are
+ * dropped and the words are matched against the cue families in the
+ * appendix's order -- binary decision (auxiliary- or modal-initial), numerical
+ * reasoning, lexical readout, entity grounding -- the first match deciding;
+ * otherwise general understanding.  The cue phrase lists are this library's
+ * reading (the appendix describes the families, not the lists).  *category
+ * uses the indices of davet_demand_prior.  Errors: EINVAL (null). */
+int davet_parse_operation(const char* query, int32_t* category /*host*/);
+
 /* Evidence envelope, Eq. (6): lower = N(p; (1-rho)B), upper = N(p;
  * [1-rho+rho d]B), with p the phase profile of Sec. 4.2 and N the rescale-and-
  * clip normaliser (exact scale: min(1, s p_t), mean = beta; beta >= 1 gives

@@ -9,7 +9,7 @@ from ._lib import (  # noqa: F401
     MAX_SEQS, EXPORTED, LIB_PATH, DavetError,
     LayerWeights, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
     davet_build_views, davet_convert, davet_demand_prior, davet_denoise_step,
-    davet_head_tiled_elems, davet_pack_head,
+    davet_head_tiled_elems, davet_pack_head, davet_parse_operation,
     davet_policy_envelope, davet_policy_step, davet_run_schedule,
     davet_step_stats, davet_unmask, davet_version, davet_view_map_sizes,
     davet_view_sizes,

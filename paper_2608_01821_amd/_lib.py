@@ -93,6 +93,7 @@ _SIGS = {
     "davet_unmask": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
                                _vp]),
     "davet_demand_prior": (C.c_double, [_i32]),
+    "davet_parse_operation": (C.c_int, [C.c_char_p, _P_i32]),
     "davet_policy_envelope": (C.c_int, [C.POINTER(Policy), _i32, _P_f64,
                                         _P_f64]),
     "davet_policy_step": (C.c_int, [C.POINTER(Policy), _i32, _i32, _P_f64,
@@ -254,6 +255,12 @@ def davet_unmask(n_seqs, L, k, conf, argmax, resp_ids, resp_masked,
 
 def davet_demand_prior(category):
     return _L.davet_demand_prior(int(category))
+
+
+def davet_parse_operation(query: str) -> int:
+    out = C.c_int32(-1)
+    _check(_L.davet_parse_operation(query.encode("utf-8"), C.byref(out)))
+    return out.value
 
 
 def davet_policy_envelope(pol: Policy, T):

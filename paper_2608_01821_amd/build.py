@@ -36,7 +36,7 @@ POLICY_FLAGS = [
 HIP_SOURCES = ["views.hip", "unmask.hip", "rowops.hip", "gemm16.hip",
                "gemm_f32.hip", "attention.hip", "step.hip", "runtime.cpp",
                "schedule.cpp"]
-POLICY_SOURCES = ["policy.cpp"]
+POLICY_SOURCES = ["policy.cpp", "parser.cpp"]
 
 
 def _run(cmd):

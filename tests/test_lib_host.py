@@ -163,3 +163,33 @@ def test_mixed_view_sizes_host():
     for bad in (dv.ViewGeom(1, 27, 64, 4, 1, 2), dv.ViewGeom(1, 27, 64, 3, 1, 1),
                 dv.ViewGeom(1, 27, 64, 3, 1, -2)):
         _expect(-2, dv.davet_view_sizes, bad)
+
+
+def test_parse_operation_paper_examples(golden_dir):
+    import json
+    import os
+    g = json.load(open(os.path.join(golden_dir,
+                                    "table_operation_examples.json")))
+    for q, cat in g["examples"]:
+        assert dv.davet_parse_operation(q) == g["categories"][cat], q
+    import ctypes as C
+    assert dv.raw().davet_parse_operation(None, C.byref(C.c_int32())) == -1
+
+
+_PARSER_WORDS = ["is", "are", "does", "can", "what", "which", "who", "where",
+                 "how", "many", "much", "number", "of", "on", "the", "a",
+                 "percentage", "%", "highest", "written", "text", "title",
+                 "date", "when", "name", "country", "city", "company",
+                 "shown", "image", "in", "this", "value", "<image>", "please",
+                 "account", "counted", "more", "than", "say", "Question:",
+                 "?", ",", "'s", "isn't", "answer", "with", "single",
+                 "word", "or", "phrase", "IS", "Who", "HOW", "sum"]
+
+
+@settings(max_examples=400, deadline=None)
+@given(st.lists(st.sampled_from(_PARSER_WORDS), max_size=12),
+       st.sampled_from([" ", "  ", "\n", "-", ""]))
+def test_parse_operation_matches_oracle(words, sep):
+    from oracle import parser
+    q = sep.join(words)
+    assert dv.davet_parse_operation(q) == parser.parse(q), q
