@@ -170,7 +170,7 @@ def setup(cfg, mode, head_layout="tiled", mixed_stride=0):
     return dict(dv=dv, W=W, mcfg=mcfg, geoms=geoms, visual=visual,
                 view_bufs=view_bufs, prompt=prompt, cu=cu, L=L, ids=ids,
                 msk=msk, ws=ws, pols=pols, fixed=fixed, sizes=sizes,
-                sample=s)
+                sample=s, mixed_stride=mixed_stride)
 
 
 def run_loop(cfg, st):
@@ -356,7 +356,7 @@ def cpu_baseline(cfg, st, n_layers_run):
     s0 = st["sample"]
     visual = synth.gen_visual(cfg, s0["n_crops"][:1])[0]
     lv_f, _ = views.build_views(visual, s0["n_crops"][0], cfg.grid, cfg.K,
-                                cfg.dtype)
+                                cfg.dtype, st.get("mixed_stride", 0))
     host = dict(embed=synth.gen_embed(cfg), head=synth.gen_head(cfg),
                 layers=[synth.gen_layer_weights(cfg, i)
                         for i in range(n_layers_run)])
