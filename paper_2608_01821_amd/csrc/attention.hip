@@ -6,9 +6,10 @@
 // 16-bit path (bf16 or fp16 operands), head_dim 128, CDNA4 matrix cores.  A
 // workgroup owns 128 queries of one head and runs SPLIT (1 or 2) groups of 4
 // wavefronts; group g takes the key tiles g, g + SPLIT, ... and each of its
-// wavefronts owns 32 queries.  Keys stream in tiles of 64 staged in LDS (K
-// row-major, V transposed); the next tile of a group is fetched into registers
-// while the current one feeds the matrix cores.  Per tile a wavefront computes
+// wavefronts owns 32 queries.  Keys stream in tiles of 64 staged in LDS, K
+// and V both row-major (the V^T fragments come from the CDNA4 transposing LDS
+// read ds_read_b64_tr_b16); the next tile of a group is fetched into
+// registers while the current one feeds the matrix cores.  Per tile a wavefront computes
 // S^T = K Q^T (2 x 8 v_mfma_f32_32x32x16 ops), so every lane holds the scores
 // of ONE query: the online-softmax rescale is a per-lane scalar and the
 // probabilities, rounded to 16 bits, are already laid out as the B operand of
@@ -29,8 +30,14 @@ constexpr int HD = 128;           // head dim of the matrix-core path
 constexpr int QT = 128;           // queries per workgroup
 constexpr int KT = 64;            // keys per tile
 constexpr int K_STRIDE = HD + 8;  // 272-byte K rows
-constexpr int V_STRIDE = KT + 4;  // 136-byte V^T rows (conflict-free b64 reads)
-constexpr int GROUP_LDS = KT * K_STRIDE + HD * V_STRIDE;   // uint16 per group
+// V rows (keys) of 160 elements: a transposing read covers 8 rows x 64 bytes,
+// and a 320-byte row stride (80 dwords, 16 mod 64) lays those 8 row pieces
+// over the 64 banks exactly twice
+constexpr int V_STRIDE = HD + 32;
+constexpr int GROUP_LDS = KT * K_STRIDE + KT * V_STRIDE;   // uint16 per group
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s* lds_v4s_ptr;
 
 __device__ __forceinline__ int remap_xcd_attn(int bid, int nwg) {
   const int full = nwg & ~7;
@@ -80,7 +87,7 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   const int q = qt * QT + wave * 32 + l32;         // this lane's query
   const int qc = min(q, N - 1);
   uint16_t* Ks = smem + grp * GROUP_LDS;
-  uint16_t* Vt = Ks + KT * K_STRIDE;
+  uint16_t* Vs = Ks + KT * K_STRIDE;       // V row-major: [key][dim]
 
   // Q^T fragments (B operand): 8 k-steps of 16 head dims
   v8 qf[HD / 16];
@@ -100,9 +107,8 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
 
   const uint16_t* kbase = qkv + (size_t)row0 * ld + d + (size_t)h * HD;
   const uint16_t* vbase = qkv + (size_t)row0 * ld + 2 * d + (size_t)h * HD;
-  constexpr int KI = KT * HD / 8 / 256;     // 16-byte K loads per thread
-  constexpr int VI = KT * HD / 16 / 256;    // key pairs of V per thread
-  u32x4 kr[KI], va[VI], vb[VI];
+  constexpr int KI = KT * HD / 8 / 256;     // 16-byte K (and V) loads per thread
+  u32x4 kr[KI], vr[KI];
   auto fetch = [&](int kb) {
     const int k0 = kb * KT;
 #pragma unroll
@@ -112,12 +118,10 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       kr[it] = *reinterpret_cast<const u32x4*>(kbase + (size_t)gk * ld + (w & 15) * 8);
     }
 #pragma unroll
-    for (int it = 0; it < VI; ++it) {
+    for (int it = 0; it < KI; ++it) {
       const int w = tg + it * 256;
-      const int kp = w >> 4, dc = w & 15;
-      const int g0 = min(k0 + 2 * kp, N - 1), g1 = min(k0 + 2 * kp + 1, N - 1);
-      va[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)g0 * ld + dc * 8);
-      vb[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)g1 * ld + dc * 8);
+      const int gk = min(k0 + (w >> 4), N - 1);
+      vr[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)gk * ld + (w & 15) * 8);
     }
   };
   auto stash = [&]() {
@@ -127,16 +131,9 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       *reinterpret_cast<u32x4*>(&Ks[(w >> 4) * K_STRIDE + (w & 15) * 8]) = kr[it];
     }
 #pragma unroll
-    for (int it = 0; it < VI; ++it) {
+    for (int it = 0; it < KI; ++it) {
       const int w = tg + it * 256;
-      const int kp = w >> 4, dc = w & 15;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = (va[it][e] & 0xffffu) | (vb[it][e] << 16);
-        const uint32_t hi = (va[it][e] >> 16) | (vb[it][e] & 0xffff0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * e) * V_STRIDE + 2 * kp]) = lo;
-        *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * e + 1) * V_STRIDE + 2 * kp]) = hi;
-      }
+      *reinterpret_cast<u32x4*>(&Vs[(w >> 4) * V_STRIDE + (w & 15) * 8]) = vr[it];
     }
   };
 
@@ -210,12 +207,23 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
 #pragma unroll
       for (int ps = 0; ps < 4; ++ps) {
-        const int kl = ps * 16 + hh * 4;
 #pragma unroll
         for (int dt = 0; dt < HD / 32; ++dt) {
-          const uint16_t* vr = &Vt[(dt * 32 + l32) * V_STRIDE + kl];
-          const u32x2 v0 = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 v1 = *reinterpret_cast<const u32x2*>(vr + 8);
+          // V^T fragment by transposing reads of the row-major tile: within
+          // each 16-lane group, lane i receives element i % 4 of the 8-byte
+          // piece addressed by group lane 4r + i / 4, for r = 0..3; group
+          // lane j therefore addresses key ks + 4*(lane / 32) + j / 4 and dims
+          // dt*32 + 16*((lane / 16) & 1) + 4*(j % 4), so lane l collects keys
+          // ks + 4*(l / 32) + r of dim dt*32 + l % 32 (ks = ps*16, +8 for the
+          // second half of the fragment)
+          const int j = lane & 15;
+          const uint16_t* vp = &Vs[(ps * 16 + hh * 4 + (j >> 2)) * V_STRIDE +
+                                   dt * 32 + 16 * ((lane >> 4) & 1) + 4 * (j & 3)];
+          const v4s t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_ptr)vp);
+          const v4s t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_v4s_ptr)(vp + 8 * V_STRIDE));
+          const u32x2 v0 = __builtin_bit_cast(u32x2, t0);
+          const u32x2 v1 = __builtin_bit_cast(u32x2, t1);
           u32x4 vv;
           vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
           u32x4 pw;
