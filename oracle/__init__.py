@@ -9,6 +9,8 @@ in ``synth`` serve both sides.
 Contents (each function cites the passage of the paper it follows):
   views   -- evidence hierarchy by per-crop average pooling + index maps
              (Sec. 4.3 "Ordered evidence hierarchy", v^(K) = v)
+  realizers -- nested pruning and hierarchical similarity merging through
+             the same index maps (Sec. 4.3 "Compatible evidence realizers")
   policy  -- phase profile, normalisation N(p; beta), evidence envelope,
              trajectory risk, envelope allocation, K-level quantisation
              (Sec. 4.2, Eqs. 6-9; Appendix A Table A for the demand prior)
@@ -25,4 +27,4 @@ equations.  Readings of silent or ambiguous passages are listed in the
 design notes of the repository and restated where each is used.
 """
 
-from . import views, policy, model, decode, stats, loop  # noqa: F401
+from . import views, realizers, policy, model, decode, stats, loop  # noqa: F401
