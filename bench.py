@@ -65,6 +65,11 @@ def parse():
                     help="middle level = the mixed view (coarse tokens plus "
                          "the raw-token lattice of stride S) instead of the "
                          "middle pooling level")
+    ap.add_argument("--realizer", choices=["pool", "prune", "merge"],
+                    default="pool",
+                    help="evidence realizer building the levels (pool: the "
+                         "paper's default; prune: nested top-n by L1 norm; "
+                         "merge: single-linkage similarity merging)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only stream MIB MiB of fp32 through a plain "
                          "elementwise copy (y = x * 1) five times and exit: "
@@ -88,7 +93,10 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
-def setup(cfg, mode, head_layout="tiled", mixed_stride=0):
+REALIZERS = {"pool": 0, "prune": 1, "merge": 2}
+
+
+def setup(cfg, mode, head_layout="tiled", mixed_stride=0, realizer="pool"):
     import numpy as np
     import torch
 
@@ -135,7 +143,7 @@ def setup(cfg, mode, head_layout="tiled", mixed_stride=0):
     tdt = torch.int16 if bf else torch.float32
     for i in range(n):
         g = dv.ViewGeom(s["n_crops"][i], cfg.grid, cfg.d, cfg.K, dtype,
-                        mixed_stride)
+                        mixed_stride, REALIZERS[realizer])
         sz = dv.davet_view_sizes(g)
         geoms.append(g)
         sizes.append(sz)
@@ -170,7 +178,7 @@ def setup(cfg, mode, head_layout="tiled", mixed_stride=0):
     return dict(dv=dv, W=W, mcfg=mcfg, geoms=geoms, visual=visual,
                 view_bufs=view_bufs, prompt=prompt, cu=cu, L=L, ids=ids,
                 msk=msk, ws=ws, pols=pols, fixed=fixed, sizes=sizes,
-                sample=s, mixed_stride=mixed_stride)
+                sample=s, mixed_stride=mixed_stride, realizer=realizer)
 
 
 def run_loop(cfg, st):
@@ -190,7 +198,7 @@ def work_per_loop(cfg, st, levels):
     es = 2 if cfg.dtype == "bf16" else 4
     w = {k: 0.0 for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down",
                           "attention", "head_gemm_flops", "head_gemm_bytes",
-                          "views_bytes")}
+                          "views_bytes", "realizer_keys_bytes")}
     for t in range(T):
         ntot = 0
         rows = 0
@@ -206,9 +214,20 @@ def work_per_loop(cfg, st, levels):
         w["gemm_down"] += cfg.n_layers * 2.0 * ntot * F * d
         w["head_gemm_flops"] += 2.0 * rows * d * V
         w["head_gemm_bytes"] += float(V * d * es + rows * d * es)
+    rz = st.get("realizer", "pool")
     for s in range(n):
         sz = st["sizes"][s]
-        w["views_bytes"] += float((sz[-1] + sum(sz[:-1])) * d * es)
+        c, G = st["sample"]["n_crops"][s], cfg.grid
+        if rz == "pool":
+            # v read once, every pooled level written once
+            w["views_bytes"] += float((sz[-1] + sum(sz[:-1])) * d * es)
+            continue
+        # keys: v read once, one float64 per token (prune) or edge (merge)
+        n_keys = sz[-1] if rz == "prune" else c * 2 * G * (G - 1)
+        w["realizer_keys_bytes"] += float(sz[-1] * d * es + 8 * n_keys)
+        # level rows: every member row read, every level token written
+        members = sum(sz[:-1]) if rz == "prune" else (cfg.K - 1) * sz[-1]
+        w["views_bytes"] += float((members + sum(sz[:-1])) * d * es)
     total_flops = sum(w[k] for k in ("gemm_qkv", "gemm_o", "gemm_gateup",
                                      "gemm_down", "attention",
                                      "head_gemm_flops"))
@@ -295,8 +314,8 @@ def kernel_rooflines(cfg, kern, work):
             ach = work["head_gemm_bytes"] / sec / 1e9
             out[name] = dict(bound="hbm", achieved=round(ach, 1), unit="GB/s",
                              frac=round(ach / PEAK_HBM_GBS, 4))
-        elif name == "views":
-            ach = work["views_bytes"] / sec / 1e9
+        elif name in ("views", "realizer_keys"):
+            ach = work[name + "_bytes"] / sec / 1e9
             out[name] = dict(bound="hbm", achieved=round(ach, 1), unit="GB/s",
                              frac=round(ach / PEAK_HBM_GBS, 4))
     return out
@@ -349,14 +368,19 @@ def cpu_baseline(cfg, st, n_layers_run):
     from threadpoolctl import threadpool_info
 
     import synth
-    from oracle import model, views
+    from oracle import model, realizers, views
 
     levels = st["levels"]
     T = cfg.steps
     s0 = st["sample"]
     visual = synth.gen_visual(cfg, s0["n_crops"][:1])[0]
-    lv_f, _ = views.build_views(visual, s0["n_crops"][0], cfg.grid, cfg.K,
-                                cfg.dtype, st.get("mixed_stride", 0))
+    if st.get("realizer", "pool") != "pool":
+        lv_f, _ = realizers.build_views(visual, s0["n_crops"][0], cfg.grid,
+                                        cfg.K, REALIZERS[st["realizer"]],
+                                        cfg.dtype)
+    else:
+        lv_f, _ = views.build_views(visual, s0["n_crops"][0], cfg.grid, cfg.K,
+                                    cfg.dtype, st.get("mixed_stride", 0))
     host = dict(embed=synth.gen_embed(cfg), head=synth.gen_head(cfg),
                 layers=[synth.gen_layer_weights(cfg, i)
                         for i in range(n_layers_run)])
@@ -415,7 +439,11 @@ def main():
 
     cfg = synth.get_config(args.config)
     mode = args.mode if cfg.dtype == "bf16" else "f32"
-    st = setup(cfg, mode, args.head_layout, args.mixed_stride)
+    if args.mixed_stride and args.realizer != "pool":
+        print("the mixed view is a pooling level: --mixed-stride needs "
+              "--realizer pool", file=sys.stderr)
+        sys.exit(2)
+    st = setup(cfg, mode, args.head_layout, args.mixed_stride, args.realizer)
     dv = st["dv"]
     for _ in range(args.warmup):
         run_loop(cfg, st)
@@ -461,7 +489,9 @@ def main():
                        mean_us=round(ms * 1e3 / c, 2) if c else 0.0)
                for k, (c, ms) in kern.items() if c}
     k_roof = kernel_rooflines(cfg, kern, work) if kern else {}
-    views_ms = kern.get("views", (0, 0.0))[1] if kern else None
+    views_ms = sum(kern.get(k, (0, 0.0))[1] for k in (
+        "views", "view_maps", "realizer_keys", "realizer_maps")) \
+        if kern else None
     levels_probe = per_level_steps(cfg, st, levels)
     cpu = None
     if not args.no_cpu_baseline:
@@ -491,8 +521,13 @@ def main():
         "config": {
             "workload": cfg.name, "model_dtype": cfg.dtype,
             "head_layout": args.head_layout if cfg.dtype == "bf16" else "rows",
+            "realizer": args.realizer,
             "middle_view": ("mixed, lattice stride %d" % args.mixed_stride
-                            if args.mixed_stride else "pooled (2x2 windows)"),
+                            if args.mixed_stride else
+                            {"pool": "pooled (2x2 windows)",
+                             "prune": "pruned (top-n by L1 norm)",
+                             "merge": "merged (single linkage)"}[
+                                 args.realizer]),
             "operands": {"f16": "fp16 x fp16 -> fp32 matrix cores, bf16 "
                                 "weights converted exactly",
                          "bf16": "bf16 x bf16 -> fp32 matrix cores",

@@ -61,11 +61,22 @@ typedef enum davet_dtype { DAVET_F32 = 0, DAVET_BF16 = 1, DAVET_F16 = 2 } davet_
 #define DAVET_MAX_LEVELS 4       /* K                                     */
 #define DAVET_MAX_RESP 1024      /* response length L                     */
 
+/* Evidence realizers (Sec. 4.3: any construction with an ordered
+ * evidence-cost hierarchy; pooling is the paper's default, pruning varies
+ * the retention ratio, merging the aggregation strength). */
+typedef enum davet_realizer {
+  DAVET_REALIZER_POOL = 0,   /* per-crop average pooling (and the mixed view) */
+  DAVET_REALIZER_PRUNE = 1,  /* nested top-n by token L1 norm                 */
+  DAVET_REALIZER_MERGE = 2   /* single-linkage merging by cosine similarity   */
+} davet_realizer;
+#define DAVET_MAX_REALIZER_GRID 64   /* grid limit of prune and merge */
+
 /* Geometry of one sample's visual encoding v: n_crops crops of grid x grid
  * tokens, each token a d-vector; v is [n_crops*grid*grid, d], crop-major, then
  * row-major inside a crop.  K ordered levels, level K-1 being v itself.
- * mixed_stride: 0 for the pooling pyramid; S >= 2 (K = 3 only) makes level 1
- * the mixed view of Sec. 4.3 (see davet_build_views). */
+ * mixed_stride: 0 for the pooling pyramid; S >= 2 (K = 3, pooling only) makes
+ * level 1 the mixed view of Sec. 4.3 (see davet_build_views).
+ * realizer: a davet_realizer; 0 (pooling) when the struct is zero-filled. */
 typedef struct davet_view_geom {
   int32_t n_crops;
   int32_t grid;
@@ -73,6 +84,7 @@ typedef struct davet_view_geom {
   int32_t K;          /* 1..DAVET_MAX_LEVELS */
   int32_t dtype;      /* davet_dtype of v and of the pooled levels */
   int32_t mixed_stride;
+  int32_t realizer;
 } davet_view_geom;
 
 /* Denoiser shape.  d = n_heads * head_dim, head_dim in {64, 128} (128 in the
@@ -144,20 +156,25 @@ const char* davet_version(void);
  * windows of side 2^(K-1-l) per crop with ceil padding:
  * n_l = n_crops * ceil(grid / 2^(K-1-l))^2; the mixed level has
  * n_1 = n_crops * (ceil(grid / 4)^2 + m^2), m = #{o, o+S, ... < grid},
- * o = S / 2.  Errors: EINVAL, ESHAPE (bad K, grid, n_crops or stride). */
+ * o = S / 2.  The prune and merge realizers keep the pooling counts n_l.
+ * Errors: EINVAL, ESHAPE (bad K, grid, n_crops, stride or realizer). */
 int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens /*host[K]*/);
 
 /* Lengths of the K member lists of davet_build_views' index maps (host
- * out[K]): n_crops * grid^2 per pyramid level, n_crops * (grid^2 + m^2) for
- * the mixed level. */
+ * out[K]): n_crops * grid^2 per pyramid or merge level (a partition of the
+ * tokens), n_crops * (grid^2 + m^2) for the mixed level, n_l per prune level
+ * (one member per kept token). */
 int davet_view_map_sizes(const davet_view_geom* g,
                          int32_t* n_members /*host[K]*/);
 
 /* Evidence hierarchy (Sec. 4.3, "Ordered evidence hierarchy"; Sec. 3.2: a full
- * budget leaves v unchanged).  Level l < K-1 token j is the mean of the
- * in-bounds tokens of its window (divisor = member count), accumulated in
+ * budget leaves v unchanged).  Pooling: level l < K-1 token j is the mean of
+ * the in-bounds tokens of its window (divisor = member count), accumulated in
  * float64 and rounded once to the view dtype.  Level K-1 is v itself: nothing
- * is written for it except its (identity) index map.
+ * is written for it except its (identity) index map.  Prune and merge: the
+ * levels given by davet_realizer_maps on davet_realizer_keys, each token the
+ * float64 mean of its members in member order, rounded once (a kept token of
+ * the prune realizer is copied unchanged).
  *   v            [n_crops*grid*grid, d] (dtype g.dtype), read only
  *   levels       HOST array of K device pointers; levels[l] receives
  *                [n_l, d] for l < K-1; levels[K-1] is ignored (may be NULL)
@@ -172,11 +189,60 @@ int davet_view_map_sizes(const davet_view_geom* g,
  * tokens (windows of side 4) followed by the raw tokens at rows and columns
  * o, o+S, o+2S, ... (o = S/2), row-major, each a one-member window copied
  * bit for bit from v.
- * Errors: EINVAL (null v / levels entry), ESHAPE (grid<1, n_crops<1, K out of
- * range, d % 8 != 0, mixed_stride 1 or < 0, or > 0 with K != 3), EDTYPE. */
+ * scratch: device memory of davet_views_scratch_bytes (NULL / 0 for pooling).
+ * Errors: EINVAL (null v / levels entry, misaligned v or level, realizer
+ * unknown), ENOMEM (scratch smaller than needed), ESHAPE (grid<1, n_crops<1,
+ * K out of range, d % 8 != 0, mixed_stride 1 or < 0, or > 0 with K != 3 or a
+ * realizer other than pooling, grid > DAVET_MAX_REALIZER_GRID for prune and
+ * merge), EDTYPE. */
 int davet_build_views(const davet_view_geom* g, const void* v,
                       void* const* levels, int32_t* const* idx_offsets,
-                      int32_t* const* idx_members, hipStream_t stream);
+                      int32_t* const* idx_members, void* scratch,
+                      size_t scratch_bytes, hipStream_t stream);
+
+/* Device scratch davet_build_views needs for a geometry (0 for pooling): the
+ * realizer keys plus the index maps of levels < K-1.  v and the level
+ * buffers must be 16-byte aligned; scratch 256-byte aligned.  The scratch is
+ * overwritten; nothing is kept in it after the stream reaches the end of
+ * the call. */
+int davet_views_scratch_bytes(const davet_view_geom* g, size_t* bytes);
+
+/* Number of keys of the prune (n_crops * grid^2, one per token) or merge
+ * (n_crops * 2 * grid * (grid - 1), one per grid edge) realizer; 0 for
+ * pooling.  Errors: EINVAL, ESHAPE. */
+int davet_realizer_key_count(const davet_view_geom* g, int32_t* n_keys);
+
+/* Realizer keys (Sec. 4.3, "Compatible evidence realizers"; the criteria
+ * are readings, the paper gives none), float64, device out[n_keys]:
+ *   prune  keys[c*grid^2 + i] = sum_j |v[c*grid^2 + i, j]|, the L1 norm of
+ *          token i of crop c (exact in any order for fp16 v with d <= 8192);
+ *   merge  keys[c*E + e] = cosine similarity of the two tokens of edge e of
+ *          crop c, dot / sqrt(|a|^2 |b|^2) (0 if either norm is 0),
+ *          E = 2*grid*(grid-1); edges (r,s)-(r,s+1) first at index
+ *          r*(grid-1) + s, then (r,s)-(r+1,s) at grid*(grid-1) + r*grid + s.
+ * v is [n_crops*grid^2, d] of g.dtype, 16-byte aligned, d % 8 == 0.
+ * Errors: EINVAL (null, misaligned, pooling realizer), ESHAPE
+ * (grid > DAVET_MAX_REALIZER_GRID), EDTYPE. */
+int davet_realizer_keys(const davet_view_geom* g, const void* v,
+                        double* keys, hipStream_t stream);
+
+/* Index maps of all K levels from given keys (device float64 [n_keys]),
+ * deterministic for identical keys.  Keys are ordered larger first, equal
+ * keys by lower index, NaN as -inf, -0 as +0.  Per crop and level l with
+ * n = ceil(grid / 2^(K-1-l))^2 tokens (the pooling counts):
+ *   prune  the n tokens first in key order, listed by index, one member
+ *          each (nested over levels);
+ *   merge  edges are taken in key order and each edge joining two groups
+ *          merges them until n groups remain, for l = K-2 down to 0
+ *          (single linkage; coarser groups are unions of finer ones);
+ *          groups listed by smallest member, members ascending.
+ * Level K-1 gets the identity map.  idx_offsets[l] ([n_l + 1]) and
+ * idx_members[l] (davet_view_map_sizes entry) are device pointers in HOST
+ * arrays of K; a NULL entry skips that level.  Errors as
+ * davet_realizer_keys. */
+int davet_realizer_maps(const davet_view_geom* g, const double* keys,
+                        int32_t* const* idx_offsets,
+                        int32_t* const* idx_members, hipStream_t stream);
 
 /* Element-type conversion of n values, rounding to nearest even (e.g. a bf16
  * checkpoint into the fp16 operand mode: exact whenever |x| >= 2^-17 and

@@ -29,7 +29,13 @@ class DavetError(RuntimeError):
 class ViewGeom(C.Structure):
     _fields_ = [("n_crops", C.c_int32), ("grid", C.c_int32), ("d", C.c_int32),
                 ("K", C.c_int32), ("dtype", C.c_int32),
-                ("mixed_stride", C.c_int32)]
+                ("mixed_stride", C.c_int32), ("realizer", C.c_int32)]
+
+
+DAVET_REALIZER_POOL = 0
+DAVET_REALIZER_PRUNE = 1
+DAVET_REALIZER_MERGE = 2
+MAX_REALIZER_GRID = 64
 
 
 class ModelCfg(C.Structure):
@@ -80,7 +86,13 @@ _SIGS = {
     "davet_view_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
     "davet_view_map_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
     "davet_build_views": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
-                                    _P_vp, _vp]),
+                                    _P_vp, _vp, C.c_size_t, _vp]),
+    "davet_views_scratch_bytes": (C.c_int, [C.POINTER(ViewGeom),
+                                            C.POINTER(C.c_size_t)]),
+    "davet_realizer_key_count": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
+    "davet_realizer_keys": (C.c_int, [C.POINTER(ViewGeom), _vp, _vp, _vp]),
+    "davet_realizer_maps": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
+                                      _vp]),
     "davet_convert": (C.c_int, [_vp, _i32, _vp, _i32, C.c_size_t, _vp]),
     "davet_head_tiled_elems": (C.c_size_t, [_i32, _i32]),
     "davet_pack_head": (C.c_int, [_vp, _vp, _i32, _i32, _i32, _vp]),
@@ -202,14 +214,49 @@ def davet_view_map_sizes(geom: ViewGeom):
     return list(out)
 
 
+def davet_views_scratch_bytes(geom):
+    out = C.c_size_t(0)
+    _check(_L.davet_views_scratch_bytes(C.byref(geom), C.byref(out)))
+    return int(out.value)
+
+
 def davet_build_views(geom, v, levels, offsets=None, members=None,
-                      stream=None):
+                      scratch=None, stream=None):
+    """``scratch``: a device tensor of davet_views_scratch_bytes bytes; when
+    None and the realizer needs one, a torch buffer on v's device."""
     K = geom.K
     lv = _ptr_array(list(levels) + [None] * (K - len(levels)))
     off = _ptr_array(offsets) if offsets is not None else None
     mem = _ptr_array(members) if members is not None else None
+    if scratch is None:
+        nb = davet_views_scratch_bytes(geom)
+        if nb:
+            import torch
+            scratch = torch.empty(nb, dtype=torch.uint8, device=v.device)
+    nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
     _check(_L.davet_build_views(C.byref(geom), _ptr(v), lv, off, mem,
-                                _stream(stream)))
+                                _ptr(scratch), nbytes, _stream(stream)))
+
+
+def davet_realizer_key_count(geom):
+    out = C.c_int32(0)
+    _check(_L.davet_realizer_key_count(C.byref(geom), C.byref(out)))
+    return int(out.value)
+
+
+def davet_realizer_keys(geom, v, keys, stream=None):
+    _check(_L.davet_realizer_keys(C.byref(geom), _ptr(v), _ptr(keys),
+                                  _stream(stream)))
+
+
+def davet_realizer_maps(geom, keys, offsets=None, members=None, stream=None):
+    K = geom.K
+    off = _ptr_array(list(offsets) + [None] * (K - len(offsets))) \
+        if offsets is not None else None
+    mem = _ptr_array(list(members) + [None] * (K - len(members))) \
+        if members is not None else None
+    _check(_L.davet_realizer_maps(C.byref(geom), _ptr(keys), off, mem,
+                                  _stream(stream)))
 
 
 def davet_convert(src, src_dtype, dst, dst_dtype, n=None, stream=None):

@@ -33,7 +33,7 @@ POLICY_FLAGS = [
     "-D__HIP_PLATFORM_AMD__",
 ]
 
-HIP_SOURCES = ["views.hip", "unmask.hip", "rowops.hip", "gemm16.hip",
+HIP_SOURCES = ["views.hip", "realizers.hip", "unmask.hip", "rowops.hip", "gemm16.hip",
                "gemm_f32.hip", "attention.hip", "step.hip", "runtime.cpp",
                "schedule.cpp"]
 POLICY_SOURCES = ["policy.cpp", "parser.cpp"]

@@ -33,7 +33,8 @@ int set_error(int status, const std::string& msg);
 enum KernelClass {
   KC_VIEWS = 0, KC_VIEW_MAPS, KC_ASSEMBLE, KC_RMSNORM, KC_GEMM_QKV, KC_ROPE,
   KC_ATTN, KC_GEMM_O, KC_GEMM_GATEUP, KC_GEMM_DOWN, KC_HEAD_PREP, KC_HEAD,
-  KC_HEAD_MERGE, KC_UNMASK, KC_GEMM_F32, KC_ATTN_F32, KC_MISC, KC_COUNT
+  KC_HEAD_MERGE, KC_UNMASK, KC_GEMM_F32, KC_ATTN_F32, KC_MISC,
+  KC_REALIZER_KEYS, KC_REALIZER_MAPS, KC_COUNT
 };
 const char* kernel_class_name(int c);
 // Brackets a launch with events when profiling is on; cheap no-op otherwise.
@@ -141,6 +142,15 @@ int launch_views(const davet_view_geom& g, const void* v, void* const* levels,
                  hipStream_t s);
 int launch_view_maps(const davet_view_geom& g, int32_t* const* offs,
                      int32_t* const* mem, hipStream_t s);
+// Geometry checks shared by every view entry point (EINVAL/ESHAPE).
+int check_view_geom(const davet_view_geom* g, const char* who);
+// Prune / merge realizers: scratch size and the whole build (keys, maps,
+// levels) into caller scratch.
+size_t realizer_scratch_bytes(const davet_view_geom& g);
+int build_views_realizer(const davet_view_geom& g, const void* v,
+                         void* const* levels, int32_t* const* offs,
+                         int32_t* const* mem, void* scratch,
+                         size_t scratch_bytes, hipStream_t s);
 
 // Packed-batch description passed by value to kernels.
 struct SeqPack {

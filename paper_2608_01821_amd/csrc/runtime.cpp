@@ -21,7 +21,7 @@ static const char* kClassNames[KC_COUNT] = {
     "views",      "view_maps", "assemble_norm", "rmsnorm",    "gemm_qkv",
     "rope",       "attention", "gemm_o",        "gemm_gateup", "gemm_down",
     "head_prep",  "head_gemm", "head_merge",    "unmask",     "gemm_f32",
-    "attention_f32", "misc"};
+    "attention_f32", "misc", "realizer_keys", "realizer_maps"};
 
 const char* kernel_class_name(int c) {
   return (c >= 0 && c < KC_COUNT) ? kClassNames[c] : "";

@@ -87,21 +87,22 @@ extern "C" int davet_run_schedule(
   schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off, &rope_off);
   char* ws = static_cast<char*>(workspace);
 
+  // a1: evidence views, once per sample (the prune / merge realizers use the
+  // start of the workspace as scratch; nothing else lives there yet)
+  for (int s = 0; s < n_seqs; ++s) {
+    std::vector<void*> lv(K, nullptr);
+    for (int l = 0; l < K - 1; ++l) lv[l] = view_bufs[(size_t)s * (K - 1) + l];
+    int rc = davet_build_views(&geoms[s], visual[s], lv.data(), nullptr,
+                               nullptr, workspace, ws_bytes, stream);
+    if (rc) return rc;
+  }
+
   // rotary table for every position of the longest sequence, once per loop
   // (a step's sequences are never longer than at the full view)
   float* rope = reinterpret_cast<float*>(ws + rope_off);
   {
     int rc = launch_rope_table((int)max_len, cfg->head_dim, cfg->rope_theta,
                                rope, stream);
-    if (rc) return rc;
-  }
-
-  // a1: evidence views, once per sample
-  for (int s = 0; s < n_seqs; ++s) {
-    std::vector<void*> lv(K, nullptr);
-    for (int l = 0; l < K - 1; ++l) lv[l] = view_bufs[(size_t)s * (K - 1) + l];
-    int rc = davet_build_views(&geoms[s], visual[s], lv.data(), nullptr,
-                               nullptr, stream);
     if (rc) return rc;
   }
 

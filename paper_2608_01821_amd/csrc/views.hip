@@ -266,14 +266,24 @@ int launch_view_maps(const davet_view_geom& g, int32_t* const* offs,
 }  // namespace davet
 
 namespace davet {
-static int check_geom(const davet_view_geom* g, const char* who) {
+int check_view_geom(const davet_view_geom* g, const char* who) {
   DAVET_CHECK_ARG(g->K >= 1 && g->K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
                   std::string(who) + ": K out of range [1, 4]");
   DAVET_CHECK_ARG(g->grid >= 1 && g->n_crops >= 1, DAVET_ESHAPE,
                   std::string(who) + ": grid and n_crops must be >= 1");
-  DAVET_CHECK_ARG(g->mixed_stride == 0 || (g->mixed_stride >= 2 && g->K == 3),
+  DAVET_CHECK_ARG(g->realizer >= DAVET_REALIZER_POOL &&
+                      g->realizer <= DAVET_REALIZER_MERGE, DAVET_EINVAL,
+                  std::string(who) + ": unknown realizer");
+  DAVET_CHECK_ARG(g->mixed_stride == 0 ||
+                      (g->mixed_stride >= 2 && g->K == 3 &&
+                       g->realizer == DAVET_REALIZER_POOL),
                   DAVET_ESHAPE,
-                  std::string(who) + ": mixed_stride must be 0, or >= 2 with K = 3");
+                  std::string(who) + ": mixed_stride must be 0, or >= 2 with "
+                  "K = 3 and the pooling realizer");
+  DAVET_CHECK_ARG(g->realizer == DAVET_REALIZER_POOL ||
+                      g->grid <= DAVET_MAX_REALIZER_GRID, DAVET_ESHAPE,
+                  std::string(who) + ": grid above DAVET_MAX_REALIZER_GRID "
+                  "for the prune / merge realizer");
   DAVET_CHECK_ARG((long long)g->n_crops * g->grid * g->grid * 2 < (1ll << 31),
                   DAVET_ESHAPE, std::string(who) + ": too many tokens");
   return DAVET_OK;
@@ -283,7 +293,7 @@ static int check_geom(const davet_view_geom* g, const char* who) {
 extern "C" int davet_view_sizes(const davet_view_geom* g, int32_t* n_tokens) {
   using namespace davet;
   DAVET_CHECK_ARG(g && n_tokens, DAVET_EINVAL, "davet_view_sizes: null argument");
-  int rc = check_geom(g, "davet_view_sizes");
+  int rc = check_view_geom(g, "davet_view_sizes");
   if (rc) return rc;
   for (int l = 0; l < g->K; ++l) {
     const int f = 1 << (g->K - 1 - l);
@@ -303,9 +313,16 @@ extern "C" int davet_view_map_sizes(const davet_view_geom* g,
   using namespace davet;
   DAVET_CHECK_ARG(g && n_members, DAVET_EINVAL,
                   "davet_view_map_sizes: null argument");
-  int rc = check_geom(g, "davet_view_map_sizes");
+  int rc = check_view_geom(g, "davet_view_map_sizes");
   if (rc) return rc;
   for (int l = 0; l < g->K; ++l) n_members[l] = g->n_crops * g->grid * g->grid;
+  if (g->realizer == DAVET_REALIZER_PRUNE) {        // one member per token
+    for (int l = 0; l + 1 < g->K; ++l) {
+      const int f = 1 << (g->K - 1 - l);
+      const int W = (g->grid + f - 1) / f;
+      n_members[l] = g->n_crops * W * W;
+    }
+  }
   if (g->mixed_stride > 0) {
     const int m = lattice_len(g->grid, g->mixed_stride);
     n_members[1] = g->n_crops * (g->grid * g->grid + m * m);
@@ -313,15 +330,26 @@ extern "C" int davet_view_map_sizes(const davet_view_geom* g,
   return DAVET_OK;
 }
 
+extern "C" int davet_views_scratch_bytes(const davet_view_geom* g,
+                                         size_t* bytes) {
+  using namespace davet;
+  DAVET_CHECK_ARG(g && bytes, DAVET_EINVAL,
+                  "davet_views_scratch_bytes: null argument");
+  int rc = check_view_geom(g, "davet_views_scratch_bytes");
+  if (rc) return rc;
+  *bytes = realizer_scratch_bytes(*g);
+  return DAVET_OK;
+}
+
 extern "C" int davet_build_views(const davet_view_geom* g, const void* v,
                                  void* const* levels,
                                  int32_t* const* idx_offsets,
-                                 int32_t* const* idx_members,
-                                 hipStream_t stream) {
+                                 int32_t* const* idx_members, void* scratch,
+                                 size_t scratch_bytes, hipStream_t stream) {
   using namespace davet;
   DAVET_CHECK_ARG(g && v, DAVET_EINVAL, "davet_build_views: null geometry or v");
   {
-    int rc = check_geom(g, "davet_build_views");
+    int rc = check_view_geom(g, "davet_build_views");
     if (rc) return rc;
   }
   DAVET_CHECK_ARG(g->d >= 8 && g->d % 8 == 0, DAVET_ESHAPE,
@@ -329,13 +357,21 @@ extern "C" int davet_build_views(const davet_view_geom* g, const void* v,
   DAVET_CHECK_ARG(g->dtype == DAVET_F32 || g->dtype == DAVET_BF16 ||
                       g->dtype == DAVET_F16, DAVET_EDTYPE,
                   "davet_build_views: dtype must be DAVET_F32, BF16 or F16");
+  DAVET_CHECK_ARG(((uintptr_t)v & 15) == 0, DAVET_EINVAL,
+                  "davet_build_views: v must be 16-byte aligned");
   if (g->K > 1) {
     DAVET_CHECK_ARG(levels != nullptr, DAVET_EINVAL,
                     "davet_build_views: levels is null");
-    for (int l = 0; l < g->K - 1; ++l)
+    for (int l = 0; l < g->K - 1; ++l) {
       DAVET_CHECK_ARG(levels[l] != nullptr, DAVET_EINVAL,
                       "davet_build_views: null pooled level pointer");
+      DAVET_CHECK_ARG(((uintptr_t)levels[l] & 15) == 0, DAVET_EINVAL,
+                      "davet_build_views: level buffers must be 16-byte aligned");
+    }
   }
+  if (g->realizer != DAVET_REALIZER_POOL)
+    return build_views_realizer(*g, v, levels, idx_offsets, idx_members,
+                                scratch, scratch_bytes, stream);
   int rc = launch_views(*g, v, levels, stream);
   if (rc != DAVET_OK) return rc;
   return launch_view_maps(*g, idx_offsets, idx_members, stream);

@@ -24,7 +24,7 @@ import torch
 
 import paper_2608_01821_amd as dv
 import synth
-from oracle import decode, model, views
+from oracle import decode, model, realizers, views
 
 TOL = {"f32": dict(logits=1e-5, gap=1e-4, conf=1e-4),
        "bf16": dict(logits=1e-2, gap=None, conf=5e-2),
@@ -60,10 +60,10 @@ def model_cfg(cfg, mode=None):
                        DTYPE[mode])
 
 
-def view_geom(cfg, n_crops, mode=None, mixed_stride=0):
+def view_geom(cfg, n_crops, mode=None, mixed_stride=0, realizer=0):
     mode = mode or default_mode(cfg)
     return dv.ViewGeom(n_crops, cfg.grid, cfg.d, cfg.K, DTYPE[mode],
-                       mixed_stride)
+                       mixed_stride, realizer)
 
 
 class Model:
@@ -107,16 +107,20 @@ class Sample:
     """One sample's inputs on both sides and its GPU-built views."""
 
     def __init__(self, cfg, n_crops, visual, prompt, mode=None,
-                 mixed_stride=0):
+                 mixed_stride=0, realizer=0):
         self.cfg = cfg
         self.mode = mode = mode or default_mode(cfg)
         dev_v, host_v = to_mode(visual, mode)
         self.visual = host_v
         self.prompt = prompt
         self.n_crops = n_crops
-        self.ref_levels, _ = views.build_views(host_v, n_crops, cfg.grid,
-                                               cfg.K, mode, mixed_stride)
-        geom = view_geom(cfg, n_crops, mode, mixed_stride)
+        if realizer:
+            self.ref_levels, _ = realizers.build_views(
+                host_v, n_crops, cfg.grid, cfg.K, realizer, mode)
+        else:
+            self.ref_levels, _ = views.build_views(host_v, n_crops, cfg.grid,
+                                                   cfg.K, mode, mixed_stride)
+        geom = view_geom(cfg, n_crops, mode, mixed_stride, realizer)
         self.sizes = dv.davet_view_sizes(geom)
         self.dev_v = torch.from_numpy(dev_v).cuda()
         tdt = torch.float32 if mode == "f32" else torch.int16

@@ -99,10 +99,11 @@ def test_argument_validation_without_gpu():
     _expect(-2, dv.davet_view_sizes, dv.ViewGeom(0, 12, 256, 3, 0))
     lib = dv.raw()
     import ctypes as C
-    assert lib.davet_build_views(C.byref(g), None, None, None, None, None) == -1
+    assert lib.davet_build_views(C.byref(g), None, None, None, None, None, 0,
+                                 None) == -1
     bad = dv.ViewGeom(1, 12, 250, 3, dv.DAVET_F32)
     assert lib.davet_build_views(C.byref(bad), C.c_void_p(16), None, None,
-                                 None, None) == -2
+                                 None, None, 0, None) == -2
     assert lib.davet_unmask(1, 32, 0, C.c_void_p(16), C.c_void_p(16),
                             C.c_void_p(16), C.c_void_p(16), None, None) == -1
     assert lib.davet_unmask(1, 2000, 2, C.c_void_p(16), C.c_void_p(16),
@@ -193,3 +194,46 @@ def test_parse_operation_matches_oracle(words, sep):
     from oracle import parser
     q = sep.join(words)
     assert dv.davet_parse_operation(q) == parser.parse(q), q
+
+
+def test_realizer_host_checks():
+    # prune / merge keep the pooling counts; their map sizes and key counts
+    # follow the documented formulas; every rejection happens before any HIP
+    # call
+    import ctypes as C
+    lib = dv.raw()
+    for rz in (dv.DAVET_REALIZER_PRUNE, dv.DAVET_REALIZER_MERGE):
+        g = dv.ViewGeom(5, 27, 4096, 3, dv.DAVET_F16, 0, rz)
+        assert dv.davet_view_sizes(g) == [245, 980, 3645]
+        sizes = dv.davet_view_map_sizes(g)
+        if rz == dv.DAVET_REALIZER_PRUNE:
+            assert sizes == [245, 980, 3645]
+            assert dv.davet_realizer_key_count(g) == 3645
+        else:
+            assert sizes == [3645, 3645, 3645]
+            assert dv.davet_realizer_key_count(g) == 5 * 2 * 27 * 26
+        assert dv.davet_views_scratch_bytes(g) > 8 * dv.davet_realizer_key_count(g)
+        # grid above the limit, mixed view with another realizer
+        _expect(-2, dv.davet_view_sizes, dv.ViewGeom(1, 65, 64, 3, 0, 0, rz))
+        _expect(-2, dv.davet_view_sizes, dv.ViewGeom(1, 27, 64, 3, 0, 2, rz))
+        # scratch missing or too small
+        lv = (C.c_void_p * 2)(256, 256)
+        assert lib.davet_build_views(C.byref(g), C.c_void_p(256), lv, None,
+                                     None, None, 0, None) == -4
+        assert lib.davet_build_views(C.byref(g), C.c_void_p(256), lv, None,
+                                     None, C.c_void_p(256), 64, None) == -4
+        # misaligned v
+        assert lib.davet_build_views(C.byref(g), C.c_void_p(8), lv, None,
+                                     None, None, 0, None) == -1
+        assert lib.davet_realizer_keys(C.byref(g), C.c_void_p(8),
+                                       C.c_void_p(256), None) == -1
+    assert dv.davet_view_sizes(dv.ViewGeom(1, 64, 64, 3, 0, 0, 2)) == \
+        [256, 1024, 4096]
+    _expect(-1, dv.davet_view_sizes, dv.ViewGeom(1, 12, 64, 3, 0, 0, 3))
+    pool = dv.ViewGeom(1, 12, 64, 3, 0)
+    assert dv.davet_views_scratch_bytes(pool) == 0
+    assert dv.davet_realizer_key_count(pool) == 0
+    assert lib.davet_realizer_keys(C.byref(pool), C.c_void_p(256),
+                                   C.c_void_p(256), None) == -1
+    assert lib.davet_realizer_maps(C.byref(pool), C.c_void_p(256), None, None,
+                                   None) == -1
