@@ -70,6 +70,15 @@ def parse():
                     help="evidence realizer building the levels (pool: the "
                          "paper's default; prune: nested top-n by L1 norm; "
                          "merge: single-linkage similarity merging)")
+    ap.add_argument("--schedule", choices=["config", "policy"],
+                    default="config",
+                    help="level schedule: the workload's own (config) or the "
+                         "allocation policy with the per-sample demand of the "
+                         "sample's operation category")
+    ap.add_argument("--crossing", action="store_true",
+                    help="policy schedules: also time the same levels as a "
+                         "fixed schedule and report the per-step cost of the "
+                         "policy's device-to-host handshake")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only stream MIB MiB of fp32 through a plain "
                          "elementwise copy (y = x * 1) five times and exit: "
@@ -438,6 +447,9 @@ def main():
     import synth
 
     cfg = synth.get_config(args.config)
+    if args.schedule == "policy" and cfg.schedule != "policy":
+        import dataclasses
+        cfg = dataclasses.replace(cfg, schedule="policy")
     mode = args.mode if cfg.dtype == "bf16" else "f32"
     if args.mixed_stride and args.realizer != "pool":
         print("the mixed view is a pooling level: --mixed-stride needs "
@@ -492,6 +504,25 @@ def main():
     views_ms = sum(kern.get(k, (0, 0.0))[1] for k in (
         "views", "view_maps", "realizer_keys", "realizer_maps")) \
         if kern else None
+    crossing = None
+    if args.crossing and st["pols"] is not None:
+        # the same levels as a fixed schedule: the difference per step is the
+        # policy's handshake (signals + allocation on the GPU, levels to host)
+        pols = st["pols"]
+        st["pols"], st["fixed"] = None, list(levels)
+        run_loop(cfg, st)
+        torch.cuda.synchronize()
+        f0 = time.perf_counter()
+        for _ in range(args.steps):
+            run_loop(cfg, st)
+        torch.cuda.synchronize()
+        fixed_ms = (time.perf_counter() - f0) / args.steps * 1e3
+        st["pols"], st["fixed"] = pols, None
+        crossing = dict(policy_ms_per_loop=round(ms_loop, 3),
+                        same_levels_fixed_ms_per_loop=round(fixed_ms, 3),
+                        us_per_step=round((ms_loop - fixed_ms) / cfg.steps
+                                          * 1e3, 2),
+                        share=round((ms_loop - fixed_ms) / ms_loop, 5))
     levels_probe = per_level_steps(cfg, st, levels)
     cpu = None
     if not args.no_cpu_baseline:
@@ -552,6 +583,7 @@ def main():
             views_ms=round(views_ms, 4), loop_ms=round(ms_loop, 3),
             share=round(views_ms / ms_loop, 6)),
         "per_level_all_masked": levels_probe,
+        "policy_crossing": crossing,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

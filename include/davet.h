@@ -11,17 +11,21 @@
  *                        [view | prompt | response] (Sec. 3.1, Eq. 1) with the
  *                        argmax / confidence decoding of masked positions
  *   davet_unmask         confidence-ranked commitment (Eq. 2)
- *   davet_policy_*       the allocation policy (Sec. 4.2, Eqs. 6-9), host-side
+ *   davet_policy_*       the allocation policy (Sec. 4.2, Eqs. 6-9): envelope
+ *                        and step on the host, the per-step closed loop also
+ *                        on the GPU (davet_policy_step_device)
  *   davet_run_schedule   the whole loop: views once, then T steps
  *
  * Conventions, for every entry point:
  *   - Pointers are DEVICE pointers unless the comment says host.  Arrays are
  *     dense and row-major.  The caller owns every buffer, including the
  *     workspace; the library never frees caller memory and allocates no device
- *     memory (davet_run_schedule may use small host-side vectors).
+ *     memory (davet_run_schedule may use small host-side vectors and, in
+ *     policy mode, a few hundred bytes of pinned host memory per call).
  *   - Device work is enqueued asynchronously on the given HIP stream.  Only
- *     davet_run_schedule in policy mode synchronises (one small device-to-host
- *     copy per step, to read the signals the risk of the next step needs).
+ *     davet_run_schedule in policy mode synchronises: once per step, on the
+ *     GPU kernel that writes the next levels (the next step's launch sizes
+ *     depend on them).
  *   - Every argument is validated before anything is enqueued; on an error the
  *     call returns a negative davet_status, enqueues nothing, and
  *     davet_last_error() describes the failure (thread-local string).
@@ -366,6 +370,26 @@ int davet_step_stats(int32_t L, const float* conf, const int32_t* argmax,
                      const int32_t* argmax_prev, const uint8_t* masked_after,
                      double* cbar, double* churn);
 
+/* The closed loop on the GPU (Sec. 4.2): davet_step_stats of every sample
+ * after step t's commitment followed by davet_policy_step for step t+1, with
+ * bit-identical results (the same float64 operations in the same order).
+ *   n_seqs samples of L response positions; 1 <= t < T.
+ *   pols, lower, upper: HOST (lower/upper [n_seqs * T] from
+ *     davet_policy_envelope, sample s at s*T); every pols[s].K equal.
+ *   conf, argmax (step t), argmax_prev (step t-1; NULL exactly when t = 1),
+ *   masked_after: DEVICE [n_seqs * L], sample-major.
+ *   level_out, budget_out (and r_out unless NULL): DEVICE or pinned host
+ *     [n_seqs], the level, b_{t+1} and r_{t+1} of each sample.
+ * Errors: EINVAL (null, t out of range, argmax_prev inconsistent with t, K
+ * differs or out of range), ESHAPE (n_seqs, L). */
+int davet_policy_step_device(int32_t n_seqs, int32_t L, int32_t t, int32_t T,
+                             const davet_policy* pols, const double* lower,
+                             const double* upper, const float* conf,
+                             const int32_t* argmax, const int32_t* argmax_prev,
+                             const uint8_t* masked_after, int32_t* level_out,
+                             double* budget_out, double* r_out,
+                             hipStream_t stream);
+
 /* ------------------------------------------------------------- schedule -- */
 
 /* The whole DAVET loop for a packed batch (Sec. 3.1 and Sec. 4; Fig. 2):
@@ -373,7 +397,10 @@ int davet_step_stats(int32_t L, const float* conf, const int32_t* argmax,
  * choose each sequence's level -- fixed_levels[s*T + t-1] when fixed_levels is
  * given, else the policy pols[s] (Eqs. 7-9) from the signals of step t-1 --
  * davet_denoise_step, davet_unmask with k.  In policy mode each step ends with
- * one device-to-host copy of conf/argmax/flags and a stream synchronisation.
+ * the device policy step (as davet_policy_step_device, writing the next
+ * levels and budgets to pinned host memory) and a stream synchronisation;
+ * the levels and budgets equal those of davet_step_stats + davet_policy_step
+ * on the same signals bit for bit.
  *   geoms: HOST [n_seqs] (d and dtype must match cfg)
  *   visual: HOST [n_seqs] device pointers to each v
  *   view_bufs: HOST [n_seqs*(K-1)] device pointers, pooled level l of

@@ -11,7 +11,8 @@ from ._lib import (  # noqa: F401
     LayerWeights, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
     davet_build_views, davet_convert, davet_demand_prior, davet_denoise_step,
     davet_head_tiled_elems, davet_pack_head, davet_parse_operation,
-    davet_policy_envelope, davet_policy_step, davet_realizer_key_count,
+    davet_policy_envelope, davet_policy_step, davet_policy_step_device,
+    davet_realizer_key_count,
     davet_realizer_keys, davet_realizer_maps, davet_run_schedule,
     davet_step_stats, davet_unmask, davet_version, davet_view_map_sizes,
     davet_view_sizes, davet_views_scratch_bytes,

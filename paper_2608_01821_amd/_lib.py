@@ -113,6 +113,10 @@ _SIGS = {
                                     _P_i32, _P_f64]),
     "davet_step_stats": (C.c_int, [_i32, C.POINTER(C.c_float), _P_i32, _P_i32,
                                    C.POINTER(C.c_uint8), _P_f64, _P_f64]),
+    "davet_policy_step_device": (C.c_int, [_i32, _i32, _i32, _i32,
+                                           C.POINTER(Policy), _P_f64, _P_f64,
+                                           _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                           _vp]),
     "davet_run_schedule": (C.c_int, [C.POINTER(ModelCfg), C.POINTER(WeightsT),
                                      _i32, C.POINTER(ViewGeom), _P_vp, _P_vp,
                                      _vp, _P_i32, _i32, _i32, _i32,
@@ -343,6 +347,23 @@ def davet_step_stats(conf, argmax, argmax_prev, masked_after):
         None if prev is None else prev.ctypes.data_as(_P_i32),
         m.ctypes.data_as(C.POINTER(C.c_uint8)), C.byref(cb), C.byref(ch)))
     return cb.value, ch.value
+
+
+def davet_policy_step_device(pols, t, T, lower, upper, conf, argmax,
+                             argmax_prev, masked_after, level_out, budget_out,
+                             r_out=None, stream=None):
+    """lower/upper: host float64 [n_seqs * T]; the other arrays are device
+    tensors ([n_seqs * L] inputs, [n_seqs] outputs)."""
+    n = len(pols)
+    L = conf.numel() // n
+    p = (Policy * n)(*pols)
+    lo = np.ascontiguousarray(lower, dtype=np.float64)
+    up = np.ascontiguousarray(upper, dtype=np.float64)
+    _check(_L.davet_policy_step_device(
+        n, L, int(t), int(T), p, lo.ctypes.data_as(_P_f64),
+        up.ctypes.data_as(_P_f64), _ptr(conf), _ptr(argmax), _ptr(argmax_prev),
+        _ptr(masked_after), _ptr(level_out), _ptr(budget_out), _ptr(r_out),
+        _stream(stream)))
 
 
 def davet_run_schedule(cfg, weights: Weights, geoms, visual, view_bufs,

@@ -34,7 +34,8 @@ POLICY_FLAGS = [
 ]
 
 HIP_SOURCES = ["views.hip", "realizers.hip", "unmask.hip", "rowops.hip", "gemm16.hip",
-               "gemm_f32.hip", "attention.hip", "step.hip", "runtime.cpp",
+               "gemm_f32.hip", "attention.hip", "step.hip", "policy_dev.hip",
+               "runtime.cpp",
                "schedule.cpp"]
 POLICY_SOURCES = ["policy.cpp", "parser.cpp"]
 

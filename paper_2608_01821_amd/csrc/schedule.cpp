@@ -1,13 +1,19 @@
 // The DAVET loop (Sec. 3.1 with Sec. 4; the procedure of Fig. 2): views are
 // built once per sample, then every step picks each sample's level (a fixed
 // schedule, or the allocation policy from the previous step's signals), runs
-// the denoiser and commits.  Policy mode reads conf/argmax/flags back once per
-// step (the only device-to-host crossing) to form the risk signals.
+// the denoiser and commits.  In policy mode the GPU forms the risk signals
+// and the next allocation after each commitment (launch_policy_step) and
+// writes the next levels and budgets into pinned host memory, then a stamp;
+// the host polls the stamp (the only crossing per step: the next step's
+// launch sizes depend on the levels) and enqueues the next step.
 
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
+#include <cstddef>
+#include <string>
 #include <vector>
 
 #include "common.h"
@@ -15,7 +21,14 @@
 namespace davet {
 void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
                       int64_t L, size_t* conf_off, size_t* argmax_off,
-                      size_t* rope_off);
+                      size_t* argmax2_off, size_t* rope_off);
+int launch_policy_step(int n_seqs, int L, int K, const double* alpha,
+                       const double* lower, const double* upper,
+                       const float* conf, const int32_t* argmax,
+                       const int32_t* argmax_prev, const uint8_t* masked_after,
+                       int32_t* level_out, double* budget_out, double* r_out,
+                       double* cbar_out, double* churn_out, int32_t* done,
+                       int32_t stamp, hipStream_t s);
 int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       int32_t n_seqs, const void* const* view_ptrs,
                       const int32_t* n_view, const int32_t* prompt_ids,
@@ -24,6 +37,29 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       int32_t* argmax_out, float* logits_out, void* workspace,
                       size_t ws_bytes, const float* rope_cs,
                       hipStream_t stream);
+
+// Waits until the GPU has published `want` to the pinned word *flag.  Polls
+// the word (its writer fences at system scope first, so the data it guards
+// is complete) and, every few thousand polls, the stream: an error on the
+// stream, or a stream that drained without the stamp, ends the wait.
+static int wait_stamp(const volatile int32_t* flag, int32_t want,
+                      hipStream_t s) {
+  for (unsigned spin = 1;; ++spin) {
+    if (*flag == want) break;
+    __builtin_ia32_pause();
+    if ((spin & 4095) == 0) {
+      const hipError_t q = hipStreamQuery(s);
+      if (q != hipSuccess && q != hipErrorNotReady)
+        return set_error(DAVET_EHIP, std::string("davet_run_schedule: ") +
+                                         hipGetErrorString(q));
+      if (q == hipSuccess && *flag != want)
+        return set_error(DAVET_EHIP, "davet_run_schedule: the policy step "
+                                     "ended without publishing its levels");
+    }
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  return DAVET_OK;
+}
 }
 
 extern "C" int davet_run_schedule(
@@ -83,8 +119,9 @@ extern "C" int davet_run_schedule(
   }
   DAVET_CHECK_ARG(ws_bytes >= need, DAVET_ENOMEM,
                   "davet_run_schedule: workspace smaller than the full-view size");
-  size_t conf_off = 0, am_off = 0, rope_off = 0;
-  schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off, &rope_off);
+  size_t conf_off = 0, am_off = 0, am2_off = 0, rope_off = 0;
+  schedule_scratch(cfg, max_tokens, n_seqs, L, &conf_off, &am_off, &am2_off,
+                   &rope_off);
   char* ws = static_cast<char*>(workspace);
 
   // a1: evidence views, once per sample (the prune / merge realizers use the
@@ -106,8 +143,19 @@ extern "C" int davet_run_schedule(
     if (rc) return rc;
   }
 
-  // policy state
-  std::vector<double> lower, upper;
+  // policy state: envelopes on the host (once per sample), the per-step
+  // signals and allocation on the GPU, the next levels in pinned memory
+  struct Mailbox {
+    int32_t level[DAVET_MAX_SEQS];
+    double budget[DAVET_MAX_SEQS];
+    int32_t done;                    // the last step whose levels are in
+  };
+  struct PinnedMailbox {
+    Mailbox* p = nullptr;
+    ~PinnedMailbox() { if (p) (void)hipHostFree(p); }
+  } mail;
+  Mailbox* mail_dev = nullptr;
+  std::vector<double> lower, upper, alpha(n_seqs), lo_t(n_seqs), up_t(n_seqs);
   if (pols) {
     lower.resize((size_t)n_seqs * T);
     upper.resize((size_t)n_seqs * T);
@@ -117,12 +165,17 @@ extern "C" int davet_run_schedule(
       int rc = davet_policy_envelope(&pols[s], T, &lower[(size_t)s * T],
                                      &upper[(size_t)s * T]);
       if (rc) return rc;
+      alpha[s] = pols[s].alpha;
+    }
+    if (T > 1) {
+      DAVET_HIP(hipHostMalloc((void**)&mail.p, sizeof(Mailbox),
+                              hipHostMallocCoherent));
+      DAVET_HIP(hipHostGetDevicePointer((void**)&mail_dev, mail.p, 0));
+      mail.p->done = 0;
     }
   }
-  std::vector<double> cbar(n_seqs, 0.0), churn(n_seqs, 0.0);
-  std::vector<float> conf_h((size_t)n_seqs * L);
-  std::vector<int32_t> am_h((size_t)n_seqs * L), am_prev((size_t)n_seqs * L);
-  std::vector<uint8_t> mask_h((size_t)n_seqs * L);
+  int32_t* am_buf[2] = {reinterpret_cast<int32_t*>(ws + am_off),
+                        reinterpret_cast<int32_t*>(ws + am2_off)};
   std::vector<const void*> vptr(n_seqs);
   std::vector<int32_t> nview(n_seqs);
 
@@ -130,11 +183,18 @@ extern "C" int davet_run_schedule(
     for (int s = 0; s < n_seqs; ++s) {
       int lv;
       double b = NAN;
-      if (pols) {
-        int rc = davet_policy_step(&pols[s], t, T, &lower[(size_t)s * T],
-                                   &upper[(size_t)s * T], cbar[s], churn[s],
-                                   &b, &lv, nullptr);
+      if (pols && t == 1) {
+        // r_1 = 1: no signal exists yet (Eq. 7)
+        int rc = davet_policy_step(&pols[s], 1, T, &lower[(size_t)s * T],
+                                   &upper[(size_t)s * T], 0.0, 0.0, &b, &lv,
+                                   nullptr);
         if (rc) return rc;
+      } else if (pols) {
+        lv = mail.p->level[s];
+        b = mail.p->budget[s];
+        DAVET_CHECK_ARG(lv >= 0 && lv < K, DAVET_EHIP,
+                        "davet_run_schedule: device policy returned a level "
+                        "out of range");
       } else {
         lv = fixed_levels[(size_t)s * T + (t - 1)];
       }
@@ -146,7 +206,7 @@ extern "C" int davet_run_schedule(
     float* conf = conf_trace ? conf_trace + (size_t)(t - 1) * n_seqs * L
                              : reinterpret_cast<float*>(ws + conf_off);
     int32_t* am = argmax_trace ? argmax_trace + (size_t)(t - 1) * n_seqs * L
-                               : reinterpret_cast<int32_t*>(ws + am_off);
+                               : am_buf[(t - 1) & 1];
     int rc = denoise_step_impl(cfg, w, n_seqs, vptr.data(), nview.data(),
                                prompt_ids, cu_prompt, resp_ids, resp_masked, L,
                                conf, am, nullptr, workspace, ws_bytes, rope,
@@ -156,20 +216,26 @@ extern "C" int davet_run_schedule(
                       stream);
     if (rc) return rc;
     if (pols && t < T) {
-      // signals of step t for the risk of step t+1 (Sec. 4.2)
-      const size_t n = (size_t)n_seqs * L;
-      DAVET_HIP(hipMemcpyAsync(conf_h.data(), conf, n * 4, hipMemcpyDeviceToHost, stream));
-      DAVET_HIP(hipMemcpyAsync(am_h.data(), am, n * 4, hipMemcpyDeviceToHost, stream));
-      DAVET_HIP(hipMemcpyAsync(mask_h.data(), resp_masked, n, hipMemcpyDeviceToHost, stream));
-      DAVET_HIP(hipStreamSynchronize(stream));
+      // signals of step t -> allocation of step t+1 (Sec. 4.2)
+      const int32_t* am_prev =
+          t == 1 ? nullptr
+                 : argmax_trace ? argmax_trace + (size_t)(t - 2) * n_seqs * L
+                                : am_buf[t & 1];
       for (int s = 0; s < n_seqs; ++s) {
-        const size_t o = (size_t)s * L;
-        rc = davet_step_stats(L, &conf_h[o], &am_h[o],
-                              t == 1 ? nullptr : &am_prev[o], &mask_h[o],
-                              &cbar[s], &churn[s]);
-        if (rc) return rc;
+        lo_t[s] = lower[(size_t)s * T + t];
+        up_t[s] = upper[(size_t)s * T + t];
       }
-      am_prev.swap(am_h);
+      char* md = reinterpret_cast<char*>(mail_dev);
+      rc = launch_policy_step(
+          n_seqs, L, K, alpha.data(), lo_t.data(), up_t.data(), conf, am,
+          am_prev, resp_masked,
+          reinterpret_cast<int32_t*>(md + offsetof(Mailbox, level)),
+          reinterpret_cast<double*>(md + offsetof(Mailbox, budget)), nullptr,
+          nullptr, nullptr,
+          reinterpret_cast<int32_t*>(md + offsetof(Mailbox, done)), t, stream);
+      if (rc) return rc;
+      rc = wait_stamp(&mail.p->done, t, stream);
+      if (rc) return rc;
     }
   }
   return DAVET_OK;

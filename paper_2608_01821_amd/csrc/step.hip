@@ -23,7 +23,7 @@
 namespace davet {
 
 struct Layout {
-  size_t conf, argmax;                 // run_schedule scratch
+  size_t conf, argmax, argmax2;        // run_schedule scratch
   size_t X, A, QKV, O, H, rope, pos, list, Hm, pmax, psum, parg, logits;
   size_t part;                         // split-K partial tiles (16-bit path)
   size_t rope_sched;                   // run_schedule's rotary table (last)
@@ -56,6 +56,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   };
   o.conf = take(rows * 4);
   o.argmax = take(rows * 4);
+  o.argmax2 = take(rows * 4);    // the schedule loop's previous predictions
   o.X = take((size_t)tokens * c.d * 4);
   o.A = take((size_t)tokens * c.d * es);
   o.QKV = take((size_t)tokens * 3 * c.d * es);
@@ -119,10 +120,11 @@ int workspace_layout_bytes(const davet_model_cfg* c, int64_t tokens,
 // Used by run_schedule to reach its scratch region.
 void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
                       int64_t L, size_t* conf_off, size_t* argmax_off,
-                      size_t* rope_off) {
+                      size_t* argmax2_off, size_t* rope_off) {
   const Layout o = make_layout(*c, tokens, seqs, L);
   *conf_off = o.conf;
   *argmax_off = o.argmax;
+  *argmax2_off = o.argmax2;
   *rope_off = o.rope_sched;
 }
 
