@@ -27,6 +27,7 @@
 //   EPI_PARTIAL  fp32 partial tile of one K split
 
 #include <algorithm>
+#include <cmath>
 #include <type_traits>
 
 #include "common.h"
@@ -469,7 +470,10 @@ using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
 using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
 using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
-constexpr int N_VARIANTS = 14;
+// 192-row tiles: fewer padded rows and a fuller last wave of workgroups for
+// sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
+using V14 = Var<192, 128, 64, 2, 4>;   // 80 KB, 2 workgroups per CU
+constexpr int N_VARIANTS = 15;
 
 int variant_bn(int tile) {
   switch (tile) {
@@ -479,13 +483,14 @@ int variant_bn(int tile) {
 }
 int variant_bm(int tile) {
   switch (tile) {
+    case 14: return 192;
     case 1: case 3: case 7: case 8: case 13: return 256;
     case 5: return 64;
     default: return 128;
   }
 }
 int variant_bk(int tile) {
-  return (tile == 4 || (tile >= 6 && tile <= 9) || tile == 12 || tile == 13) ? 64 : 32;
+  return (tile == 4 || (tile >= 6 && tile <= 9) || tile >= 12) ? 64 : 32;
 }
 
 template <typename Fmt, int EPI>
@@ -507,6 +512,7 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
     case 11: LV(V11);
     case 12: LV(V12);
     case 13: LV(V13);
+    case 14: LV(V14);
     default: LV(V0);
   }
 #undef LV
@@ -530,22 +536,43 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 
 // Kernel choice.  For the projections of a d = 4096, ffn = 12288 layer the
 // plan is a table measured on MI355X with the weights and activations cold in
-// the last-level cache (as inside a denoising step), by token-count bucket:
-// the fastest (tile variant, K split) of a sweep over every variant and split
-// in {1, 2, 4, 8}, the split-K reduction included.  Bucket upper bounds:
-constexpr int kBuckets[] = {300, 470, 700, 1100, 1700, 2600, 1 << 30};
-constexpr int kNB = 7;
-struct TableShape { int N, K; GemmPlan plan[kNB]; };
+// the last-level cache (as inside a denoising step) at 26 token counts: the
+// fastest (tile variant, K split) of a sweep over the variants 6, 8, 12, 13,
+// 14 and splits {1, 2, 3, 4, 6, 8}, the split-K reduction included (a
+// variant replaced the previous choice only when more than 3 % faster).
+// Because the number of row tiles and of waves of workgroups changes in
+// steps, the best plan is jagged in M; a product of M rows takes the plan of
+// the nearest sample point in log M.
+constexpr int kPointM[] = {209, 300, 356, 420, 480, 565, 650, 750, 889,
+                           960, 1100, 1300, 1500, 1700, 2048, 2300, 2600,
+                           2916, 3092, 3300, 3645, 3965, 5000, 8000, 12000,
+                           18020};
+constexpr int kNP = 26;
+struct TableShape { int N, K; GemmPlan plan[kNP]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4, 0}, {13, 2, 0}, {12, 1, 0}, {13, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {12288, 4096, {{8, 4, 0}, {14, 2, 0}, {13, 2, 0}, {13, 2, 0}, {13, 2, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 2, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8, 0}, {6, 4, 0}, {6, 2, 0}, {6, 2, 0}, {12, 1, 0}, {12, 1, 0}, {13, 1, 0}}},
+    {4096, 4096, {{6, 8, 0}, {6, 8, 0}, {6, 4, 0}, {6, 4, 0}, {12, 4, 0}, {6, 3, 0}, {14, 4, 0}, {14, 4, 0}, {6, 2, 0}, {6, 2, 0}, {8, 3, 0}, {14, 2, 0}, {14, 2, 0}, {12, 1, 0}, {12, 1, 0}, {14, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2, 0}, {13, 1, 0}, {12, 1, 0}, {12, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {24576, 4096, {{8, 2, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{12, 8, 0}, {8, 8, 0}, {8, 4, 0}, {8, 4, 0}, {8, 2, 0}, {8, 2, 0}, {13, 1, 0}}},
+    {4096, 12288, {{12, 8, 0}, {14, 8, 0}, {14, 8, 0}, {8, 8, 0}, {8, 8, 0}, {12, 3, 0}, {14, 4, 0}, {14, 4, 0}, {8, 4, 0}, {8, 4, 0}, {13, 3, 0}, {14, 2, 0}, {14, 2, 0}, {8, 2, 0}, {8, 2, 0}, {8, 3, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
 };
+
+// Point i serves the rows up to the geometric mean of points i and i+1.
+static int point_index(int M) {
+  int i = 0;
+  while (i + 1 < kNP && (double)M * M > (double)kPointM[i] * kPointM[i + 1]) ++i;
+  return i;
+}
+static int point_top(int i) {            // largest M served by point i
+  if (i + 1 >= kNP) return 1 << 30;
+  int m = (int)std::sqrt((double)kPointM[i] * kPointM[i + 1]);
+  while ((double)(m + 1) * (m + 1) <= (double)kPointM[i] * kPointM[i + 1]) ++m;
+  while ((double)m * m > (double)kPointM[i] * kPointM[i + 1]) --m;
+  return m;
+}
 
 static const TableShape* table_shape(int N, int K) {
   for (const TableShape& t : kTable)
@@ -571,17 +598,14 @@ static GemmPlan plan_generic(int M, int N, int K) {
 }
 
 GemmPlan plan_gemm16(int M, int N, int K) {
-  if (const TableShape* t = table_shape(N, K)) {
-    int b = 0;
-    while (M >= kBuckets[b]) ++b;
-    return t->plan[b];
-  }
+  if (const TableShape* t = table_shape(N, K)) return t->plan[point_index(M)];
   return plan_generic(M, N, K);
 }
 
 // Largest split-K partial buffer (bytes) any M <= max_M needs.  Table shapes:
-// the bound is reached at the top of a bucket (or at max_M).  Other shapes:
-// tiles * ksplit < 512 caps it at 512 tiles of at most 256 x 256.
+// within the range a point serves the size grows with M, so the bound is
+// reached at the top of a range (or at max_M).  Other shapes: tiles * ksplit
+// < 512 caps it at 512 tiles of at most 256 x 256.
 size_t gemm16_partial_bound(int max_M, int N, int K) {
   size_t best = 0;
   auto at = [&](int m) {
@@ -590,7 +614,7 @@ size_t gemm16_partial_bound(int max_M, int N, int K) {
     if (p.ksplit > 1) best = std::max(best, (size_t)p.ksplit * m * N * 4);
   };
   if (table_shape(N, K)) {
-    for (int b = 0; b < kNB; ++b) at(std::min(max_M, kBuckets[b] - 1));
+    for (int i = 0; i < kNP; ++i) at(std::min(max_M, point_top(i)));
     at(max_M);
     return best;
   }
