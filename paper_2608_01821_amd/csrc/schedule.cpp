@@ -35,7 +35,7 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       const int32_t* cu_prompt, const int32_t* resp_ids,
                       const uint8_t* resp_masked, int32_t L, float* conf_out,
                       int32_t* argmax_out, float* logits_out, void* workspace,
-                      size_t ws_bytes, const float* rope_cs,
+                      size_t ws_bytes, const float* rope_cs, int rows_bound,
                       hipStream_t stream);
 
 // Waits until the GPU has published `want` to the pinned word *flag.  Polls
@@ -207,10 +207,14 @@ extern "C" int davet_run_schedule(
                              : reinterpret_cast<float*>(ws + conf_off);
     int32_t* am = argmax_trace ? argmax_trace + (size_t)(t - 1) * n_seqs * L
                                : am_buf[(t - 1) & 1];
+    // every step commits min(k, masked) positions per sequence, so before
+    // step t at most max(0, L - k(t-1)) of a sequence's positions are masked
+    const int64_t per_seq = std::max<int64_t>(0, (int64_t)L - (int64_t)k * (t - 1));
+    const int rows_bound = (int)std::max<int64_t>(1, per_seq * n_seqs);
     int rc = denoise_step_impl(cfg, w, n_seqs, vptr.data(), nview.data(),
                                prompt_ids, cu_prompt, resp_ids, resp_masked, L,
                                conf, am, nullptr, workspace, ws_bytes, rope,
-                               stream);
+                               rows_bound, stream);
     if (rc) return rc;
     rc = davet_unmask(n_seqs, L, k, conf, am, resp_ids, resp_masked, nullptr,
                       stream);

@@ -150,7 +150,7 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       const int32_t* cu_prompt, const int32_t* resp_ids,
                       const uint8_t* resp_masked, int32_t L, float* conf_out,
                       int32_t* argmax_out, float* logits_out, void* workspace,
-                      size_t ws_bytes, const float* rope_cs,
+                      size_t ws_bytes, const float* rope_cs, int rows_bound,
                       hipStream_t stream);
 }  // namespace davet
 
@@ -168,11 +168,15 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
   return davet::denoise_step_impl(cfg, w, n_seqs, view_ptrs, n_view,
                                   prompt_ids, cu_prompt, resp_ids, resp_masked,
                                   L, conf_out, argmax_out, logits_out,
-                                  workspace, ws_bytes, nullptr, stream);
+                                  workspace, ws_bytes, nullptr, n_seqs * L,
+                                  stream);
 }
 
 // rope_cs: a rotary table already holding every position this step uses
 // (the schedule loop's); null: build it in the step's own region.
+// rows_bound: an upper bound on the masked positions the caller knows on the
+// host (n_seqs * L when it knows none); it only sizes the head's grid, whose
+// workgroups still loop over any live rows beyond it.
 int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                              int32_t n_seqs, const void* const* view_ptrs,
                              const int32_t* n_view, const int32_t* prompt_ids,
@@ -181,7 +185,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                              float* conf_out, int32_t* argmax_out,
                              float* logits_out, void* workspace,
                              size_t ws_bytes, const float* rope_cs,
-                             hipStream_t stream) {
+                             int rows_bound, hipStream_t stream) {
   using namespace davet;
   int rc = check_cfg(cfg);
   if (rc) return rc;
@@ -358,7 +362,8 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
     RUN(launch_head16(dt, (const uint16_t*)Hm, (const uint16_t*)w->head, list,
                       rows, c.vocab, d, c.mask_id, pmax, psum, parg,
                       logits_out, s, -1, -1,
-                      w->head_layout == DAVET_HEAD_TILED));
+                      w->head_layout == DAVET_HEAD_TILED,
+                      (std::max(1, std::min(rows, rows_bound)) + 127) / 128));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {

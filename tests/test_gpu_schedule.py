@@ -203,3 +203,29 @@ def test_run_schedule_policy_ragged(cid):
         assert ref["trace"]["budgets"][0] == bu[i, 0]
         assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
                                         i) >= 1
+
+
+def test_run_schedule_head_over_several_row_tiles():
+    """Five sequences of 100 response positions: the vocabulary head sees up
+    to 500 masked rows, so the schedule sizes its grid for several 128-row
+    tiles per vocabulary slab; every sequence still matches the oracle."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_any_config(12), resp_len=100, k=40,
+                              steps=3)
+    mdl = Model(cfg)
+    s = synth.gen_sample(cfg)
+    p = cfg.policy
+    pols = [dv.Policy(p["B"], p["rho"], p["alpha"], dv.davet_demand_prior(c),
+                      1 if p["early"] else 0, cfg.K) for c in s["categories"]]
+    lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
+    _check_invariants(cfg, ctr, atr, ids, msk)
+    assert cfg.n_seqs * cfg.resp_len > 3 * 128
+    for i, pol in enumerate(pols):
+        ref = loop.run_sequence(cfg, mdl.host,
+                                to_mode(s["visual"][i], mdl.mode)[1],
+                                s["n_crops"][i], s["prompts"][i], cfg.steps,
+                                cfg.k, pol=p, demand=dv.davet_demand_prior(
+                                    s["categories"][i]), out_dtype=mdl.mode)
+        assert ref["trace"]["levels"][0] == lv[i, 0]
+        assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
+                                        i) >= 1
