@@ -229,7 +229,9 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
                   float* logits_out, hipStream_t s, int variant = -1,
                   int krot = -1, int tiled = 0, int m_slots = 1);
-int head16_slabs(int vocab);
+// vocabulary slabs per row (pmax/psum/parg columns) the head launch with
+// this variant (-1: the default) and layout writes; at most ceil(V / 128)
+int head16_slabs(int vocab, int variant = -1, int tiled = 0);
 int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     float* C, int M, int N, int K, int ldc, int cls,
                     const int32_t* m_count, hipStream_t s);

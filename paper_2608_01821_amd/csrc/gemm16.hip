@@ -77,8 +77,10 @@ struct EpiArgs {
   // K order: N tile nb starts at slab (nb * krot) mod nk and wraps, so that
   // concurrent workgroups stream different DRAM regions (0: in order)
   int krot;
-  // B is a tiled vocabulary head (BN = 128, BK = 64 only): tile (kt, nb) is a
-  // contiguous row-major [128][64] block at (kt * n_tiles_n + nb) * 8192
+  // B is a tiled vocabulary head of 128 x 64 blocks (davet_pack_head).  1:
+  // BN = 128, BK = 64, tile (kt, nb) is the contiguous block at
+  // (kt * n_tiles_n + nb) * 8192.  2: BN a multiple of 128, BK = 32: slab
+  // step kt reads columns (kt % 2) * 32 .. +32 of block chunk kt / 2.
   int b_tiled;
 };
 
@@ -206,11 +208,17 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     } else {
       gn = min(n0 + r, N - 1);
     }
-    b_src[q] = ep.b_tiled
-                   ? B + ((size_t)kt0 * n_ntiles + nb) * BN * BK + (size_t)r * BK + c * 8
-                   : base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
+    if (ep.b_tiled == 2)
+      b_src[q] = B + ((size_t)min(nb * (BN / 128) + (r >> 7), (N - 1) >> 7) * 128 +
+                      (r & 127)) * 64 + c * 8;
+    else
+      b_src[q] = ep.b_tiled
+                     ? B + ((size_t)kt0 * n_ntiles + nb) * BN * BK + (size_t)r * BK + c * 8
+                     : base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
   }
-  const size_t b_kstride = ep.b_tiled ? (size_t)n_ntiles * BN * BK : (size_t)BK;
+  const size_t b_kstride =
+      ep.b_tiled == 2 ? (size_t)((N + 127) / 128) * 128 * 64
+      : ep.b_tiled   ? (size_t)n_ntiles * BN * BK : (size_t)BK;
 
   // A load instructions of this wave holding at least one live row: rows
   // past the last live one are not fetched (their LDS rows feed only output
@@ -228,9 +236,12 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int q = 0; q < AI; ++q)
       if (q < na) dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
+    const size_t boff = ep.b_tiled == 2
+                            ? (size_t)((kt0 + kt) >> 1) * b_kstride + ((kt0 + kt) & 1) * 32
+                            : (size_t)kt * b_kstride;
 #pragma unroll
     for (int q = 0; q < BI; ++q)
-      dma16(b_src[q] + (size_t)kt * b_kstride, sb + (wave * BI + q) * 1024);
+      dma16(b_src[q] + boff, sb + (wave * BI + q) * 1024);
   };
 
   f32x16 acc[TM][TN];
@@ -473,11 +484,12 @@ using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
 // 192-row tiles: fewer padded rows and a fuller last wave of workgroups for
 // sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
 using V14 = Var<192, 128, 64, 2, 4>;   // 80 KB, 2 workgroups per CU
-constexpr int N_VARIANTS = 15;
+using V15 = Var<128, 256, 32, 3, 8>;   // 72 KB: tiled vocabulary head
+constexpr int N_VARIANTS = 16;
 
 int variant_bn(int tile) {
   switch (tile) {
-    case 2: case 3: case 8: case 9: case 13: return 256;
+    case 2: case 3: case 8: case 9: case 13: case 15: return 256;
     default: return 128;
   }
 }
@@ -651,7 +663,19 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
              : gemm_dispatch<BF16>(plan, epi, A, B, B2, M, N, K, ep, s);
 }
 
-int head16_slabs(int vocab) { return (vocab + 127) / 128; }
+// The head kernel a launch runs: the tiled layout streams 256-column slabs
+// 32 deep (two packed 128-row blocks per workgroup, so each activation tile
+// is read half as often as with 128-column slabs; measured on MI355X at
+// V = 126464, d = 4096: 188 -> 181 us at 2 live rows, 262 -> 232 at 128),
+// the row-major layout 128 x 128 tiles with 8 wavefronts.
+static int head16_variant(int variant, int tiled) {
+  return variant >= 0 ? variant : (tiled ? 15 : 12);
+}
+
+int head16_slabs(int vocab, int variant, int tiled) {
+  const int bn = head16_variant(variant, tiled) == 15 ? 256 : 128;
+  return (vocab + bn - 1) / bn;
+}
 
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
@@ -661,7 +685,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   // 8 wavefronts on the 128 x 128 tile: the matrix work of a slab is spread
   // over twice the waves, so it hides behind the other workgroup's stream
   // (measured on MI355X: 201 -> 187 us at 2 live rows, 214 -> 192 at 64)
-  if (variant < 0) variant = 12;
+  variant = head16_variant(variant, tiled);
   // K-order rotation per vocabulary slab: helps the weight stream of an
   // isolated head launch on MI355X but not inside the denoising step (the
   // measured default there is 0, every slab starting at k = 0)
@@ -672,16 +696,15 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   ep.list = list;
   ep.vocab = vocab;
   ep.mask_id = mask_id;
-  ep.n_slabs = head16_slabs(vocab);
+  ep.n_slabs = head16_slabs(vocab, variant, tiled);
   ep.pmax = pmax;
   ep.psum = psum;
   ep.parg = parg;
   ep.logits_out = logits_out;
   ep.krot = krot;
-  ep.b_tiled = tiled;
-  if (tiled && ((variant != 6 && variant != 12) || d % 64))
+  ep.b_tiled = tiled ? (variant == 15 ? 2 : 1) : 0;
+  if (tiled && ((variant != 6 && variant != 12 && variant != 15) || d % 64))
     return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
-  // 128-column slabs (BN = 128) keep n_slabs = ceil(V / 128)
   // m_slots M slots per vocabulary slab: a workgroup loops over the live row
   // tiles mb, mb + m_slots, ...  The caller sizes m_slots from a bound on the
   // live rows it knows on the host (the schedule loop's: at most L - k(t-1)
@@ -694,6 +717,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
     switch (variant) {
       case 0: HV(F16, V0);
       case 12: HV(F16, V12);
+      case 15: HV(F16, V15);
       case 10: HV(F16, V10);
       case 11: HV(F16, V11);
       default: HV(F16, V6);
@@ -701,6 +725,8 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   }
   switch (variant) {
     case 0: HV(BF16, V0);
+    case 12: HV(BF16, V12);
+    case 15: HV(BF16, V15);
     case 10: HV(BF16, V10);
     case 11: HV(BF16, V11);
     default: HV(BF16, V6);

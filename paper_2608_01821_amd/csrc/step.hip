@@ -355,7 +355,8 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
                                c.dtype, Hm, s));
   if (bf) {
-    const int slabs = head16_slabs(c.vocab);
+    const int slabs =
+        head16_slabs(c.vocab, -1, w->head_layout == DAVET_HEAD_TILED);
     float* pmax = reinterpret_cast<float*>(ws + lay.pmax);
     float* psum = reinterpret_cast<float*>(ws + lay.psum);
     int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);

@@ -215,3 +215,27 @@ def compare(cfg, tol, masked, g_conf, g_am, g_logits, pos, ref_lg, ref_am,
     check_decode(g_am[pos], g_conf[pos], ref_lg, ref_am, ref_cf, cfg.mask_id,
                  gap, tol["conf"])
     return err
+
+
+# The tiled head reduces each row over 256-column vocabulary slabs, the
+# row-major head over 128-column ones: the logits are the same bits (same
+# products, same K order), the confidence is the same softmax maximum with
+# its fp32 sum of exponentials grouped differently.  Along each path of an
+# online-softmax reduction tree a level adds at most one rounding of the add
+# (2^-24 relative) and one rescale by exp(m_old - m_new) (__expf, within
+# 2 ulp: 2^-22); both trees are under 48 levels deep at V <= 2^17 (a lane's
+# columns, 5 shuffle levels, 2 wave halves, the slab merge), so the two
+# results lie within 2 * 48 * 5 * 2^-24 < 3e-5 of each other.
+CONF_REGROUP_RTOL = 3e-5
+
+
+def assert_conf_regrouped(a, b):
+    """Confidences from the two head layouts: -inf (committed rows) at the
+    same places, finite values within CONF_REGROUP_RTOL."""
+    a = np.asarray(a)
+    b = np.asarray(b)
+    fa, fb = np.isfinite(a), np.isfinite(b)
+    assert np.array_equal(fa, fb)
+    assert np.array_equal(a[~fa], b[~fb])
+    rel = np.abs(a[fa].astype(np.float64) - b[fb]) / np.abs(b[fb])
+    assert rel.size == 0 or rel.max() <= CONF_REGROUP_RTOL, rel.max()
