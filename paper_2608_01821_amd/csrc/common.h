@@ -228,7 +228,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
                   float* logits_out, hipStream_t s, int variant = -1,
-                  int krot = -1, int tiled = 0, int m_slots = 1);
+                  int krot = -1, int tiled = 0, int live_bound = -1);
 // vocabulary slabs per row (pmax/psum/parg columns) the head launch with
 // this variant (-1: the default) and layout writes; at most ceil(V / 128)
 int head16_slabs(int vocab, int variant = -1, int tiled = 0);

@@ -502,6 +502,7 @@ int variant_bm(int tile) {
   }
 }
 int variant_bk(int tile) {
+  if (tile == 15) return 32;
   return (tile == 4 || (tile >= 6 && tile <= 9) || tile >= 12) ? 64 : 32;
 }
 
@@ -681,7 +682,7 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
                   float* logits_out, hipStream_t s, int variant, int krot,
-                  int tiled, int m_slots) {
+                  int tiled, int live_bound) {
   // 8 wavefronts on the 128 x 128 tile: the matrix work of a slab is spread
   // over twice the waves, so it hides behind the other workgroup's stream
   // (measured on MI355X: 201 -> 187 us at 2 live rows, 214 -> 192 at 64)
@@ -706,12 +707,15 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   if (tiled && ((variant != 6 && variant != 12 && variant != 15) || d % 64))
     return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
   // m_slots M slots per vocabulary slab: a workgroup loops over the live row
-  // tiles mb, mb + m_slots, ...  The caller sizes m_slots from a bound on the
-  // live rows it knows on the host (the schedule loop's: at most L - k(t-1)
-  // per sequence), so one slot per live tile streams a slab's weights from
-  // HBM once (the tiles of a slab sit on one XCD and share its L2), and late
-  // steps with few masked rows launch no idle workgroups.
-  m_slots = std::max(1, std::min(m_slots, (max_rows + 127) / 128));
+  // tiles mb, mb + m_slots, ...  m_slots covers live_bound, a bound on the
+  // live rows the caller knows on the host (the schedule loop's: at most
+  // L - k(t-1) per sequence; a looser bound is still correct), so one slot
+  // per live tile streams a slab's weights from HBM once (the tiles of a slab
+  // sit on one XCD and share its L2), and late steps with few masked rows
+  // launch no idle workgroups.
+  const int bm = variant_bm(variant);
+  const int live = live_bound < 0 ? max_rows : std::min(max_rows, live_bound);
+  const int m_slots = std::max(1, (live + bm - 1) / bm);
 #define HV(Fmt, Vn) return launch_tiles<Fmt, Vn, EPI_HEAD>(Hm, W, nullptr, max_rows, vocab, d, 1, ep, s, m_slots)
   if (dtype == DAVET_F16) {
     switch (variant) {

@@ -364,7 +364,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       rows, c.vocab, d, c.mask_id, pmax, psum, parg,
                       logits_out, s, -1, -1,
                       w->head_layout == DAVET_HEAD_TILED,
-                      (std::max(1, std::min(rows, rows_bound)) + 127) / 128));
+                      std::max(1, std::min(rows, rows_bound))));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {
