@@ -230,8 +230,10 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   float* logits_out, hipStream_t s, int variant = -1,
                   int krot = -1, int tiled = 0, int live_bound = -1);
 // vocabulary slabs per row (pmax/psum/parg columns) the head launch with
-// this variant (-1: the default) and layout writes; at most ceil(V / 128)
-int head16_slabs(int vocab, int variant = -1, int tiled = 0);
+// this variant (-1: the default for the layout and the live-row bound)
+// writes; at most ceil(V / 128)
+int head16_slabs(int vocab, int variant = -1, int tiled = 0,
+                 int live_bound = 1);
 int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     float* C, int M, int N, int K, int ldc, int cls,
                     const int32_t* m_count, hipStream_t s);

@@ -79,8 +79,9 @@ struct EpiArgs {
   int krot;
   // B is a tiled vocabulary head of 128 x 64 blocks (davet_pack_head).  1:
   // BN = 128, BK = 64, tile (kt, nb) is the contiguous block at
-  // (kt * n_tiles_n + nb) * 8192.  2: BN a multiple of 128, BK = 32: slab
-  // step kt reads columns (kt % 2) * 32 .. +32 of block chunk kt / 2.
+  // (kt * n_tiles_n + nb) * 8192.  2: BN a multiple of 128, BK 32 or 64: slab
+  // step kt reads BK columns of each of its BN / 128 blocks in chunk
+  // kt * BK / 64, from column kt * BK % 64.
   int b_tiled;
 };
 
@@ -236,9 +237,9 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int q = 0; q < AI; ++q)
       if (q < na) dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
-    const size_t boff = ep.b_tiled == 2
-                            ? (size_t)((kt0 + kt) >> 1) * b_kstride + ((kt0 + kt) & 1) * 32
-                            : (size_t)kt * b_kstride;
+    const int kel = (kt0 + kt) * BK;       // first K element of the slab
+    const size_t boff = ep.b_tiled == 2 ? (size_t)(kel >> 6) * b_kstride + (kel & 63)
+                                        : (size_t)kt * b_kstride;
 #pragma unroll
     for (int q = 0; q < BI; ++q)
       dma16(b_src[q] + boff, sb + (wave * BI + q) * 1024);
@@ -664,17 +665,27 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
              : gemm_dispatch<BF16>(plan, epi, A, B, B2, M, N, K, ep, s);
 }
 
-// The head kernel a launch runs: the tiled layout streams 256-column slabs
-// 32 deep (two packed 128-row blocks per workgroup, so each activation tile
-// is read half as often as with 128-column slabs; measured on MI355X at
-// V = 126464, d = 4096: 188 -> 181 us at 2 live rows, 262 -> 232 at 128),
-// the row-major layout 128 x 128 tiles with 8 wavefronts.
-static int head16_variant(int variant, int tiled) {
-  return variant >= 0 ? variant : (tiled ? 15 : 12);
+// The head kernel a launch runs, for a bound `live` on its live rows.  The
+// tiled layout streams 256-column slabs: while at most 128 rows (or an odd
+// number of 128-row tiles up to five) are live, 128 x 256 tiles with a
+// 32-deep ring (V15: each activation tile re-read for half as many slabs as
+// with 128-column slabs, one round of 494 workgroups; measured on MI355X at
+// V = 126464, d = 4096: 188 -> 181 us at 2 live rows, 262 -> 232 at 128
+// against 128 x 128 tiles); otherwise the head is bound by its matrix work
+// and takes the 256 x 256 projection tile (V13; 192 rows 369 -> 295 us, 1024
+// rows 1361 -> 1198, 2048 rows 2835 -> 2433), whose cost steps with every
+// 256 rows where V15's steps with every 128.  Both read the same columns per
+// lane, so logits and slab partials are the same bits whichever runs.  The
+// row-major layout takes 128 x 128 tiles with 8 wavefronts.
+static int head16_variant(int variant, int tiled, int live) {
+  if (variant >= 0) return variant;
+  if (!tiled) return 12;
+  const int n128 = (std::max(live, 1) + 127) / 128;
+  return (n128 == 1 || (n128 % 2 == 1 && n128 <= 5)) ? 15 : 13;
 }
 
-int head16_slabs(int vocab, int variant, int tiled) {
-  const int bn = head16_variant(variant, tiled) == 15 ? 256 : 128;
+int head16_slabs(int vocab, int variant, int tiled, int live_bound) {
+  const int bn = variant_bn(head16_variant(variant, tiled, live_bound));
   return (vocab + bn - 1) / bn;
 }
 
@@ -683,10 +694,12 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
                   float* logits_out, hipStream_t s, int variant, int krot,
                   int tiled, int live_bound) {
-  // 8 wavefronts on the 128 x 128 tile: the matrix work of a slab is spread
-  // over twice the waves, so it hides behind the other workgroup's stream
-  // (measured on MI355X: 201 -> 187 us at 2 live rows, 214 -> 192 at 64)
-  variant = head16_variant(variant, tiled);
+  // Row-major head: 8 wavefronts on the 128 x 128 tile (V12 over V6): the
+  // matrix work of a slab is spread over twice the waves, so it hides behind
+  // the other workgroup's stream (measured on MI355X: 201 -> 187 us at 2 live
+  // rows, 214 -> 192 at 64)
+  const int live = live_bound < 0 ? max_rows : std::min(max_rows, live_bound);
+  variant = head16_variant(variant, tiled, live);
   // K-order rotation per vocabulary slab: helps the weight stream of an
   // isolated head launch on MI355X but not inside the denoising step (the
   // measured default there is 0, every slab starting at k = 0)
@@ -697,14 +710,15 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   ep.list = list;
   ep.vocab = vocab;
   ep.mask_id = mask_id;
-  ep.n_slabs = head16_slabs(vocab, variant, tiled);
+  ep.n_slabs = head16_slabs(vocab, variant, tiled, live);
   ep.pmax = pmax;
   ep.psum = psum;
   ep.parg = parg;
   ep.logits_out = logits_out;
   ep.krot = krot;
-  ep.b_tiled = tiled ? (variant == 15 ? 2 : 1) : 0;
-  if (tiled && ((variant != 6 && variant != 12 && variant != 15) || d % 64))
+  const bool wide = variant == 8 || variant == 13 || variant == 15;
+  ep.b_tiled = tiled ? (wide ? 2 : 1) : 0;
+  if (tiled && ((variant != 6 && variant != 12 && !wide) || d % 64))
     return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
   // m_slots M slots per vocabulary slab: a workgroup loops over the live row
   // tiles mb, mb + m_slots, ...  m_slots covers live_bound, a bound on the
@@ -714,27 +728,26 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
   // sit on one XCD and share its L2), and late steps with few masked rows
   // launch no idle workgroups.
   const int bm = variant_bm(variant);
-  const int live = live_bound < 0 ? max_rows : std::min(max_rows, live_bound);
   const int m_slots = std::max(1, (live + bm - 1) / bm);
 #define HV(Fmt, Vn) return launch_tiles<Fmt, Vn, EPI_HEAD>(Hm, W, nullptr, max_rows, vocab, d, 1, ep, s, m_slots)
+#define HEAD_VARIANTS(Fmt)       \
+  switch (variant) {             \
+    case 0: HV(Fmt, V0);         \
+    case 6: HV(Fmt, V6);         \
+    case 8: HV(Fmt, V8);         \
+    case 10: HV(Fmt, V10);       \
+    case 11: HV(Fmt, V11);       \
+    case 12: HV(Fmt, V12);       \
+    case 13: HV(Fmt, V13);       \
+    case 15: HV(Fmt, V15);       \
+  }
   if (dtype == DAVET_F16) {
-    switch (variant) {
-      case 0: HV(F16, V0);
-      case 12: HV(F16, V12);
-      case 15: HV(F16, V15);
-      case 10: HV(F16, V10);
-      case 11: HV(F16, V11);
-      default: HV(F16, V6);
-    }
+    HEAD_VARIANTS(F16)
+  } else {
+    HEAD_VARIANTS(BF16)
   }
-  switch (variant) {
-    case 0: HV(BF16, V0);
-    case 12: HV(BF16, V12);
-    case 15: HV(BF16, V15);
-    case 10: HV(BF16, V10);
-    case 11: HV(BF16, V11);
-    default: HV(BF16, V6);
-  }
+  return set_error(DAVET_EINVAL, "head16: no such head variant");
+#undef HEAD_VARIANTS
 #undef HV
 }
 

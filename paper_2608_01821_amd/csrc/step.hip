@@ -355,16 +355,15 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
                                c.dtype, Hm, s));
   if (bf) {
-    const int slabs =
-        head16_slabs(c.vocab, -1, w->head_layout == DAVET_HEAD_TILED);
+    const bool tiled = w->head_layout == DAVET_HEAD_TILED;
+    const int live = std::max(1, std::min(rows, rows_bound));
+    const int slabs = head16_slabs(c.vocab, -1, tiled, live);
     float* pmax = reinterpret_cast<float*>(ws + lay.pmax);
     float* psum = reinterpret_cast<float*>(ws + lay.psum);
     int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);
     RUN(launch_head16(dt, (const uint16_t*)Hm, (const uint16_t*)w->head, list,
                       rows, c.vocab, d, c.mask_id, pmax, psum, parg,
-                      logits_out, s, -1, -1,
-                      w->head_layout == DAVET_HEAD_TILED,
-                      std::max(1, std::min(rows, rows_bound))));
+                      logits_out, s, -1, -1, tiled, live));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {

@@ -41,12 +41,20 @@ def test_pack_head_matches_formula(vocab, d):
     assert np.array_equal(dst.cpu().numpy(), exp)
 
 
-@pytest.mark.parametrize("cid", [11, 12])
-def test_tiled_head_step(cid):
+# (config, sequences, response length, masked fraction): the last three pack
+# 200, 300 and 500 response rows, so the head runs its 256 x 256 tile over one
+# and two row slots and its 128 x 256 tile over three
+@pytest.mark.parametrize("cid,n_seqs,L,frac", [
+    (11, 3, None, 0.6), (12, 3, None, 0.6), (12, 5, 40, 1.0),
+    (12, 6, 50, 0.9), (12, 5, 100, 0.8)])
+def test_tiled_head_step(cid, n_seqs, L, frac):
+    import dataclasses
     cfg = synth.get_any_config(cid)
+    if L is not None:
+        cfg = dataclasses.replace(cfg, resp_len=L, n_seqs=n_seqs)
     mdl = Model(cfg)
     s = synth.gen_sample(cfg)
-    n_seqs = min(cfg.n_seqs, 3)
+    n_seqs = min(cfg.n_seqs, n_seqs)
     samples = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i])
                for i in range(n_seqs)]
     tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
@@ -55,7 +63,7 @@ def test_tiled_head_step(cid):
     w_tiled = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
                          head_layout=dv.DAVET_HEAD_TILED)
     rng = np.random.default_rng(cid)
-    st = [random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.6)
+    st = [random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, frac)
           for _ in samples]
     ids = np.stack([a for a, _ in st])
     masked = np.stack([b for _, b in st])
