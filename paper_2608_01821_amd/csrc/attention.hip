@@ -6,10 +6,13 @@
 // 16-bit path (bf16 or fp16 operands), head_dim 128, CDNA4 matrix cores.  A
 // workgroup owns 128 queries of one head and runs SPLIT (1 or 2) groups of 4
 // wavefronts; group g takes the key tiles g, g + SPLIT, ... and each of its
-// wavefronts owns 32 queries.  Keys stream in tiles of 64 staged in LDS, K
-// and V both row-major (the V^T fragments come from the CDNA4 transposing LDS
-// read ds_read_b64_tr_b16); the next tile of a group is fetched into
-// registers while the current one feeds the matrix cores.  Per tile a wavefront computes
+// wavefronts owns 32 queries.  Keys stream in tiles of 64: global->LDS DMA
+// moves each K and V tile row-major into one of two LDS buffers per group
+// (16-byte chunks XOR-swizzled per row, so no padding is needed for
+// conflict-free reads; the V^T fragments come from the CDNA4 transposing LDS
+// read ds_read_b64_tr_b16), the next tile landing in the other buffer while
+// the current one feeds the matrix cores, with one barrier per tile.  Per
+// tile a wavefront computes
 // S^T = K Q^T (2 x 8 v_mfma_f32_32x32x16 ops), so every lane holds the scores
 // of ONE query: the online-softmax rescale is a per-lane scalar and the
 // probabilities, rounded to 16 bits, are already laid out as the B operand of
@@ -29,15 +32,23 @@ namespace {
 constexpr int HD = 128;           // head dim of the matrix-core path
 constexpr int QT = 128;           // queries per workgroup
 constexpr int KT = 64;            // keys per tile
-constexpr int K_STRIDE = HD + 8;  // 272-byte K rows
-// V rows (keys) of 160 elements: a transposing read covers 8 rows x 64 bytes,
-// and a 320-byte row stride (80 dwords, 16 mod 64) lays those 8 row pieces
-// over the 64 banks exactly twice
-constexpr int V_STRIDE = HD + 32;
-constexpr int GROUP_LDS = KT * K_STRIDE + KT * V_STRIDE;   // uint16 per group
+constexpr int TILE_U16 = KT * HD;            // one 64 x 128 K or V tile
+constexpr int BUF_U16 = 2 * TILE_U16;        // K and V of one key tile
+constexpr int GROUP_LDS = 2 * BUF_U16;       // two buffers: 64 KB per group
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s* lds_v4s_ptr;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_ptr)lds, 16, 0, 0);
+}
+// 16-byte chunk slot of chunk c of key row r.  K: XOR by r % 16, so the 16
+// rows a fragment read touches at one chunk cover all 64 banks.  V: XOR by
+// 4 (r % 4), moving whole 64-byte groups, so the 64-byte row pieces of four
+// consecutive keys that a transposing read takes cover all banks.
+__device__ __forceinline__ int k_slot(int r, int c) { return c ^ (r & 15); }
+__device__ __forceinline__ int v_slot(int r, int c) { return c ^ ((r & 3) << 2); }
 
 __device__ __forceinline__ int remap_xcd_attn(int bid, int nwg) {
   const int full = nwg & ~7;
@@ -65,13 +76,13 @@ __global__ void __launch_bounds__(256 * SPLIT, SPLIT == 1 ? 2 : 1)
 attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
               SeqPack sp, int n_heads, int n_tiles, float scale_log2) {
   using v8 = typename Fmt::v8;
-  // SPLIT groups' K/V^T tiles; after the loop the same bytes hold the merge
-  // (merge: O as [4 waves][4][16][64 lanes] floats, then max and normaliser
-  // as [4][64] floats each)
+  // SPLIT groups' double-buffered K/V tiles; after the loop the same bytes
+  // hold the merge (O as [4 waves][4][16][64 lanes] floats, then max and
+  // normaliser as [4][64] floats each)
   constexpr int MERGE_U16 = SPLIT == 2 ? 2 * (QT * HD + 2 * 256) : 0;
   constexpr int LDS_U16 = SPLIT * GROUP_LDS > MERGE_U16 ? SPLIT * GROUP_LDS
                                                         : MERGE_U16;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[LDS_U16];
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[LDS_U16];
   const int logical = remap_xcd_attn(blockIdx.x, gridDim.x);
   const int h = logical / n_tiles;
   int s, qt;
@@ -81,13 +92,13 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   const int row0 = sp.row0[s];
   const int N = sp.row0[s + 1] - row0;
   const int t = threadIdx.x;
-  const int grp = t >> 8, tg = t & 255;
-  const int lane = t & 63, wave = (t >> 6) & 3;
+  const int grp = t >> 8;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((t >> 6) & 3);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int q = qt * QT + wave * 32 + l32;         // this lane's query
+  const int q = qt * QT + wave * 32 + l32;
   const int qc = min(q, N - 1);
-  uint16_t* Ks = smem + grp * GROUP_LDS;
-  uint16_t* Vs = Ks + KT * K_STRIDE;       // V row-major: [key][dim]
+  char* gbuf = reinterpret_cast<char*>(smem + grp * GROUP_LDS);
 
   // Q^T fragments (B operand): 8 k-steps of 16 head dims
   v8 qf[HD / 16];
@@ -107,46 +118,36 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
 
   const uint16_t* kbase = qkv + (size_t)row0 * ld + d + (size_t)h * HD;
   const uint16_t* vbase = qkv + (size_t)row0 * ld + 2 * d + (size_t)h * HD;
-  constexpr int KI = KT * HD / 8 / 256;     // 16-byte K (and V) loads per thread
-  u32x4 kr[KI], vr[KI];
-  auto fetch = [&](int kb) {
+  // tile kb into buffer b: wave w moves rows 16w .. 16w+15 of K and of V, four
+  // rows (1 KB) per load instruction; keys past the end repeat the last one
+  auto issue = [&](int kb, int b) {
+    char* kd = gbuf + b * (BUF_U16 * 2);
+    char* vd = kd + TILE_U16 * 2;
     const int k0 = kb * KT;
 #pragma unroll
-    for (int it = 0; it < KI; ++it) {
-      const int w = tg + it * 256;
-      const int gk = min(k0 + (w >> 4), N - 1);
-      kr[it] = *reinterpret_cast<const u32x4*>(kbase + (size_t)gk * ld + (w & 15) * 8);
-    }
-#pragma unroll
-    for (int it = 0; it < KI; ++it) {
-      const int w = tg + it * 256;
-      const int gk = min(k0 + (w >> 4), N - 1);
-      vr[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)gk * ld + (w & 15) * 8);
-    }
-  };
-  auto stash = [&]() {
-#pragma unroll
-    for (int it = 0; it < KI; ++it) {
-      const int w = tg + it * 256;
-      *reinterpret_cast<u32x4*>(&Ks[(w >> 4) * K_STRIDE + (w & 15) * 8]) = kr[it];
-    }
-#pragma unroll
-    for (int it = 0; it < KI; ++it) {
-      const int w = tg + it * 256;
-      *reinterpret_cast<u32x4*>(&Vs[(w >> 4) * V_STRIDE + (w & 15) * 8]) = vr[it];
+    for (int qi = 0; qi < 4; ++qi) {
+      const int r = (wave * 4 + qi) * 4 + (lane >> 4);
+      const size_t go = (size_t)min(k0 + r, N - 1) * ld;
+      dma16(kbase + go + k_slot(r, lane & 15) * 8, kd + (wave * 4 + qi) * 1024);
+      dma16(vbase + go + v_slot(r, lane & 15) * 8, vd + (wave * 4 + qi) * 1024);
     }
   };
 
   const int n_kt = (N + KT - 1) / KT;
   const int n_it = (n_kt + SPLIT - 1) / SPLIT;     // same for every group
-  if (grp < n_kt) fetch(grp);
+  if (grp < n_kt) issue(grp, 0);
   for (int it = 0; it < n_it; ++it) {
     const int kb = it * SPLIT + grp;
     const bool have = kb < n_kt;
-    if (have) stash();
-    __syncthreads();
-    if (kb + SPLIT < n_kt) fetch(kb + SPLIT);      // in flight during compute
+    // this wave's loads of tile kb have landed and its reads of the other
+    // buffer are done; after the barrier, so are every wave's
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
     if (have) {
+      const char* Kb = gbuf + (it & 1) * (BUF_U16 * 2);
+      const char* Vb = Kb + TILE_U16 * 2;
       const int k0 = kb * KT;
       // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
       f32x16 sc[2];
@@ -154,11 +155,11 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
+        const int r = mt * 32 + l32;
 #pragma unroll
         for (int ks = 0; ks < HD / 16; ++ks) {
-          const v8 kf = __builtin_bit_cast(
-              v8, *reinterpret_cast<const u32x4*>(
-                      &Ks[(mt * 32 + l32) * K_STRIDE + ks * 16 + hh * 8]));
+          const v8 kf = *reinterpret_cast<const v8*>(
+              Kb + r * 256 + (k_slot(r, ks * 2 + hh) << 4));
           sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
         }
       }
@@ -203,7 +204,6 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
       }
-
       // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
 #pragma unroll
       for (int ps = 0; ps < 4; ++ps) {
@@ -215,13 +215,15 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
           // lane j therefore addresses key ks + 4*(lane / 32) + j / 4 and dims
           // dt*32 + 16*((lane / 16) & 1) + 4*(j % 4), so lane l collects keys
           // ks + 4*(l / 32) + r of dim dt*32 + l % 32 (ks = ps*16, +8 for the
-          // second half of the fragment)
+          // second half of the fragment); an 8-byte piece never crosses a
+          // 16-byte chunk, so the swizzle moves it whole
           const int j = lane & 15;
-          const uint16_t* vp = &Vs[(ps * 16 + hh * 4 + (j >> 2)) * V_STRIDE +
-                                   dt * 32 + 16 * ((lane >> 4) & 1) + 4 * (j & 3)];
+          const int r = ps * 16 + hh * 4 + (j >> 2);
+          const int dd = dt * 32 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+          const char* vp = Vb + r * 256 + (v_slot(r, dd >> 3) << 4) + (dd & 7) * 2;
           const v4s t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_ptr)vp);
           const v4s t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4s_ptr)(vp + 8 * V_STRIDE));
+              (lds_v4s_ptr)(vp + 8 * 256));
           const u32x2 v0 = __builtin_bit_cast(u32x2, t0);
           const u32x2 v1 = __builtin_bit_cast(u32x2, t1);
           u32x4 vv;
@@ -235,13 +237,14 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
         }
       }
     }
-    __syncthreads();
   }
 
   if constexpr (SPLIT == 2) {
-    // group 1 hands (max, normaliser, O) of each query to group 0
-    float* mo = reinterpret_cast<float*>(smem);          // [4][4][16][64]
-    float* ml = mo + QT * HD;                              // [4][64] x 2
+    // group 1 hands (max, normaliser, O) of each query to group 0, once both
+    // groups are done with their tiles
+    __syncthreads();
+    float* mo = reinterpret_cast<float*>(smem);
+    float* ml = mo + QT * HD;
     if (grp == 1) {
 #pragma unroll
       for (int dt = 0; dt < HD / 32; ++dt)
