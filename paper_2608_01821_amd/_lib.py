@@ -150,8 +150,13 @@ def _check(status):
 
 
 def _ptr(t):
-    """Device (or host) address of a tensor, or None."""
-    return None if t is None else C.c_void_p(t.data_ptr())
+    """Device (or host) address of a tensor, or None.  The library reads
+    every buffer as dense, so a strided view is refused."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("davet: tensor arguments must be contiguous")
+    return C.c_void_p(t.data_ptr())
 
 
 def _stream(stream):
@@ -163,11 +168,21 @@ def _stream(stream):
     return C.c_void_p(stream.cuda_stream)
 
 
+def _addr(t):
+    """Integer address of a dense tensor, or None."""
+    p = _ptr(t)
+    return None if p is None else p.value
+
+
 def _ptr_array(items):
     arr = (C.c_void_p * max(1, len(items)))()
     for i, t in enumerate(items):
-        arr[i] = None if t is None else (t if isinstance(t, int)
-                                         else t.data_ptr())
+        if t is None or isinstance(t, int):
+            arr[i] = t
+        else:
+            if not t.is_contiguous():
+                raise ValueError("davet: tensor arguments must be contiguous")
+            arr[i] = t.data_ptr()
     return arr
 
 
@@ -191,15 +206,11 @@ class Weights:
         self._layers = (LayerWeights * max(1, len(layers)))()
         for i, lw in enumerate(layers):
             self._layers[i] = LayerWeights(
-                lw["wqkv"].data_ptr(), lw["wo"].data_ptr(),
-                lw["wg"].data_ptr(), lw["wu"].data_ptr(), lw["wd"].data_ptr(),
-                lw["attn_norm"].data_ptr() if lw.get("attn_norm") is not None
-                else None,
-                lw["ffn_norm"].data_ptr() if lw.get("ffn_norm") is not None
-                else None)
-        self.struct = WeightsT(embed.data_ptr(), head.data_ptr(),
-                               final_norm.data_ptr() if final_norm is not None
-                               else None, self._layers, int(head_layout))
+                _addr(lw["wqkv"]), _addr(lw["wo"]), _addr(lw["wg"]),
+                _addr(lw["wu"]), _addr(lw["wd"]), _addr(lw.get("attn_norm")),
+                _addr(lw.get("ffn_norm")))
+        self.struct = WeightsT(_addr(embed), _addr(head), _addr(final_norm),
+                               self._layers, int(head_layout))
 
 
 def davet_version():

@@ -237,3 +237,20 @@ def test_realizer_host_checks():
                                    C.c_void_p(256), None) == -1
     assert lib.davet_realizer_maps(C.byref(pool), C.c_void_p(256), None, None,
                                    None) == -1
+
+
+def test_binding_refuses_strided_tensors():
+    """The library reads every buffer as dense: the binding refuses a strided
+    view instead of passing its storage address."""
+    import torch
+    from paper_2608_01821_amd import _lib
+    x = torch.zeros(4, 6)
+    assert _lib._ptr(x).value == x.data_ptr()
+    assert _lib._ptr(None) is None
+    with pytest.raises(ValueError):
+        _lib._ptr(x.t())
+    with pytest.raises(ValueError):
+        _lib._ptr_array([x, x[:, 1]])
+    lw = dict(wqkv=x, wo=x, wg=x, wu=x, wd=x.t())
+    with pytest.raises(ValueError):
+        dv.Weights(x, x, [lw])
