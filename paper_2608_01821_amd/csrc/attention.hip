@@ -7,12 +7,13 @@
 // workgroup owns 128 queries of one head and runs SPLIT (1 or 2) groups of 4
 // wavefronts; group g takes the key tiles g, g + SPLIT, ... and each of its
 // wavefronts owns 32 queries.  Keys stream in tiles of 64: global->LDS DMA
-// moves each K and V tile row-major into one of two LDS buffers per group
-// (16-byte chunks XOR-swizzled per row, so no padding is needed for
-// conflict-free reads; the V^T fragments come from the CDNA4 transposing LDS
-// read ds_read_b64_tr_b16), the next tile landing in the other buffer while
-// the current one feeds the matrix cores, with one barrier per tile.  Per
-// tile a wavefront computes
+// moves each K and V tile row-major into LDS (16-byte chunks XOR-swizzled per
+// row, so no padding is needed for conflict-free reads; the V^T fragments
+// come from the CDNA4 transposing LDS read ds_read_b64_tr_b16).  With two
+// groups each has two buffers, the next tile landing in one while the other
+// feeds the matrix cores; with one group a single buffer lets three
+// workgroups share a CU and overlap each other's loads.  Per tile a
+// wavefront computes
 // S^T = K Q^T (2 x 8 v_mfma_f32_32x32x16 ops), so every lane holds the scores
 // of ONE query: the online-softmax rescale is a per-lane scalar and the
 // probabilities, rounded to 16 bits, are already laid out as the B operand of
@@ -34,7 +35,6 @@ constexpr int QT = 128;           // queries per workgroup
 constexpr int KT = 64;            // keys per tile
 constexpr int TILE_U16 = KT * HD;            // one 64 x 128 K or V tile
 constexpr int BUF_U16 = 2 * TILE_U16;        // K and V of one key tile
-constexpr int GROUP_LDS = 2 * BUF_U16;       // two buffers: 64 KB per group
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s* lds_v4s_ptr;
@@ -71,14 +71,31 @@ __device__ __forceinline__ void locate_tile(const SeqPack& sp, int tile,
   qt = tile - acc;
 }
 
+// One key group (enough workgroups for the chip), fp16: a single K/V buffer
+// per workgroup (32 KB) so three workgroups share a CU and hide each other's
+// loads (bf16 rounding needs more registers than three waves per SIMD
+// leave: it spills there, so it keeps two buffers at two per CU).  Two key
+// groups (few workgroups): two buffers per group, the next tile landing
+// during compute.
 template <typename Fmt, int SPLIT>
-__global__ void __launch_bounds__(256 * SPLIT, SPLIT == 1 ? 2 : 1)
+constexpr int attn_bufs() {
+  return SPLIT == 1 && Fmt::dtype == DAVET_F16 ? 1 : 2;
+}
+template <typename Fmt, int SPLIT>
+constexpr int attn_minb() {
+  return SPLIT == 2 ? 1 : attn_bufs<Fmt, SPLIT>() == 1 ? 3 : 2;
+}
+
+template <typename Fmt, int SPLIT>
+__global__ void __launch_bounds__(256 * SPLIT, (attn_minb<Fmt, SPLIT>()))
 attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
               SeqPack sp, int n_heads, int n_tiles, float scale_log2) {
   using v8 = typename Fmt::v8;
   // SPLIT groups' double-buffered K/V tiles; after the loop the same bytes
   // hold the merge (O as [4 waves][4][16][64 lanes] floats, then max and
   // normaliser as [4][64] floats each)
+  constexpr int BUFS = attn_bufs<Fmt, SPLIT>();
+  constexpr int GROUP_LDS = BUFS * BUF_U16;
   constexpr int MERGE_U16 = SPLIT == 2 ? 2 * (QT * HD + 2 * 256) : 0;
   constexpr int LDS_U16 = SPLIT * GROUP_LDS > MERGE_U16 ? SPLIT * GROUP_LDS
                                                         : MERGE_U16;
@@ -139,14 +156,15 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   for (int it = 0; it < n_it; ++it) {
     const int kb = it * SPLIT + grp;
     const bool have = kb < n_kt;
-    // this wave's loads of tile kb have landed and its reads of the other
-    // buffer are done; after the barrier, so are every wave's
+    // this wave's loads of tile kb have landed (and, with two buffers, its
+    // reads of the other one are done); after the barrier, so are every wave's
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
+    if constexpr (BUFS == 2)
+      if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
     if (have) {
-      const char* Kb = gbuf + (it & 1) * (BUF_U16 * 2);
+      const char* Kb = gbuf + (BUFS == 2 ? (it & 1) : 0) * (BUF_U16 * 2);
       const char* Vb = Kb + TILE_U16 * 2;
       const int k0 = kb * KT;
       // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
@@ -236,6 +254,13 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
                               __builtin_bit_cast(v8, pw), o[dt]);
         }
       }
+    }
+    if constexpr (BUFS == 1) {
+      // every wave is done reading the buffer: refill it
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (kb + SPLIT < n_kt) issue(kb + SPLIT, 0);
     }
   }
 
@@ -339,9 +364,11 @@ int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
   const dim3 grid(tiles * n_heads);
   // Few workgroups (short sequences): two key groups per workgroup so each
-  // SIMD still holds two wavefronts.  Enough workgroups for two per CU: one
-  // key group each (measured on MI355X: 3805 tokens 477 -> 443 us, 18020
-  // tokens 8.45 -> 7.61 ms; 889 tokens 36 vs 41 us the other way).
+  // SIMD still holds two wavefronts.  Enough workgroups to fill the CUs: one
+  // key group each, three workgroups per CU (measured on MI355X against two
+  // groups: 3805 tokens 477 -> 443 us, 18020 tokens 8.45 -> 7.61 ms; 889
+  // tokens 36 vs 41 us the other way; one buffer at three workgroups per CU
+  // against two at two: 3805 tokens 325 -> 313 us, 18020 5.69 -> 5.42 ms).
   const bool split = tiles * n_heads < 512;
 #define ATTN(F)                                                                \
   if (split)                                                                   \
