@@ -177,8 +177,11 @@ int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
                       hipStream_t s);
 int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
                 const SeqPack& sp, const float* cs, hipStream_t s);
+// masked-row list (count in list[0]) and, if slot is given, each response
+// position's index in it (-1: committed)
 int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
-                     float* conf_out, int32_t* argmax_out, hipStream_t s);
+                     float* conf_out, int32_t* argmax_out, int32_t* slot,
+                     hipStream_t s);
 int launch_final_norm_gather(const float* X, const SeqPack& sp,
                              const int32_t* list, int max_rows, int d,
                              const float* gain, float eps, int dtype, void* Hm,
@@ -217,6 +220,12 @@ size_t gemm16_partial_bound(int max_M, int N, int K);
 int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,
                            int d, float* X, const float* gain, float eps,
                            void* A, hipStream_t s);
+//   X[r] += sum_s P[s][r]; then Hm[slot] = RMSNorm(X[r]) * gain for a masked
+//   response row r (the last layer's final norm and gather)
+int launch_reduce_add_gather(int dtype, const float* P, int ksplit, int rows,
+                             int d, float* X, const SeqPack& sp,
+                             const int32_t* slot, const float* gain, float eps,
+                             void* Hm, hipStream_t s);
 //   out16[r][c] = rope(sum_s P[s][r][c]) for c < rope_cols, plain otherwise
 int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
                              int ncols, int rope_cols, const int32_t* pos,

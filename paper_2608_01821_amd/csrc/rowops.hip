@@ -212,13 +212,14 @@ rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
 }
 
 // Single workgroup: ordered list of masked response positions (global index
-// s*L + i) with the count in list[0]; committed positions get conf = -inf and
-// argmax = -1.  Each thread takes a contiguous run of positions; the run
-// offsets come from a workgroup prefix sum (wavefront scan + LDS).
+// s*L + i) with the count in list[0], and (if slot is given) each position's
+// index in that list, -1 for committed ones; committed positions get conf =
+// -inf and argmax = -1.  Each thread takes a contiguous run of positions; the
+// run offsets come from a workgroup prefix sum (wavefront scan + LDS).
 __global__ void __launch_bounds__(kThreads)
 head_prep_kernel(int total, const uint8_t* __restrict__ masked,
                  int32_t* __restrict__ list, float* __restrict__ conf_out,
-                 int32_t* __restrict__ argmax_out) {
+                 int32_t* __restrict__ argmax_out, int32_t* __restrict__ slot) {
   __shared__ int wsum[kThreads / 64];
   const int per = (total + kThreads - 1) / kThreads;
   const int lo = min(total, (int)threadIdx.x * per);
@@ -244,8 +245,10 @@ head_prep_kernel(int total, const uint8_t* __restrict__ masked,
   int o = base + incl - c;
   for (int i = lo; i < hi; ++i) {
     if (masked[i]) {
+      if (slot) slot[i] = o;
       list[1 + o++] = i;
     } else {
+      if (slot) slot[i] = -1;
       conf_out[i] = -INFINITY;
       argmax_out[i] = -1;
     }
@@ -413,6 +416,44 @@ reduce_add_norm_kernel(const float* __restrict__ P, int rows, int d,
   norm_store<Fmt>(v, ss, d, gain, eps, A + (size_t)row * d, red);
 }
 
+// X[row] += sum_k P[k][row]; a masked response row also gets
+// Hm[slot] = RMSNorm(X[row]) * gain (slot: its index in the masked-row list):
+// the final norm and gather of the masked rows, fused into the split-K
+// reduction of the last layer.
+template <typename Fmt, int KS, typename T = typename Fmt::st>
+__global__ void __launch_bounds__(kThreads)
+reduce_add_gather_kernel(const float* __restrict__ P, int rows, int d,
+                         float* __restrict__ X, SeqPack sp,
+                         const int32_t* __restrict__ slot,
+                         const float* __restrict__ gain, float eps,
+                         T* __restrict__ Hm) {
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const size_t stride = (size_t)rows * d;
+  const int nc = d / 8;
+  float v[kMaxChunks][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int n = 0; n < kMaxChunks; ++n) {
+    const int c = threadIdx.x + n * kThreads;
+    if (c < nc) {
+      float* xr = X + (size_t)row * d + c * 8;
+      load8f(xr, v[n]);
+      sum_parts<KS>(P + (size_t)row * d + c * 8, stride, v[n]);
+      store8f(xr, v[n]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss += v[n][i] * v[n][i];
+    }
+  }
+  // the same for every thread of the workgroup: the row's response index
+  const int s = find_seq(sp, row);
+  const int i = row - (sp.row0[s] + sp.nview[s] + sp.plen[s]);
+  if (i < 0 || i >= sp.L) return;
+  const int j = slot[s * sp.L + i];
+  if (j < 0) return;
+  norm_store<Fmt>(v, ss, d, gain, eps, Hm + (size_t)j * d, red);
+}
+
 // columns < rope_cols hold heads of 128 dims rotated as (i, i + 64)
 template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
@@ -566,6 +607,19 @@ int launch_reduce_add_norm(int dtype, const float* P, int ksplit, int rows,
   return DAVET_OK;
 }
 
+int launch_reduce_add_gather(int dtype, const float* P, int ksplit, int rows,
+                             int d, float* X, const SeqPack& sp,
+                             const int32_t* slot, const float* gain, float eps,
+                             void* Hm, hipStream_t s) {
+  if (rows <= 0) return DAVET_OK;
+  ProfScope ps(KC_RMSNORM, s);
+  DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
+      (reduce_add_gather_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P,
+      rows, d, X, sp, slot, gain, eps, (F::st*)Hm)));
+  DAVET_HIP(hipGetLastError());
+  return DAVET_OK;
+}
+
 int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
                              int ncols, int rope_cols, const int32_t* pos,
                              const float* cs, void* out, hipStream_t s) {
@@ -651,10 +705,12 @@ int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
 }
 
 int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
-                     float* conf_out, int32_t* argmax_out, hipStream_t s) {
+                     float* conf_out, int32_t* argmax_out, int32_t* slot,
+                     hipStream_t s) {
   ProfScope ps(KC_HEAD_PREP, s);
   hipLaunchKernelGGL(head_prep_kernel, dim3(1), dim3(kThreads), 0, s,
-                     sp.n_seqs * sp.L, masked, list, conf_out, argmax_out);
+                     sp.n_seqs * sp.L, masked, list, conf_out, argmax_out,
+                     slot);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }

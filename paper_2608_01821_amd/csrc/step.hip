@@ -24,7 +24,7 @@ namespace davet {
 
 struct Layout {
   size_t conf, argmax, argmax2;        // run_schedule scratch
-  size_t X, A, QKV, O, H, rope, pos, list, Hm, pmax, psum, parg, logits;
+  size_t X, A, QKV, O, H, rope, pos, list, slot, Hm, pmax, psum, parg, logits;
   size_t part;                         // split-K partial tiles (16-bit path)
   size_t rope_sched;                   // run_schedule's rotary table (last)
   size_t total;
@@ -65,6 +65,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   o.rope = take((size_t)tokens * (c.head_dim / 2) * 8);
   o.pos = take((size_t)tokens * 4);
   o.list = take((size_t)(rows + 1) * 4);
+  o.slot = take((size_t)rows * 4);
   o.Hm = take((size_t)rows * c.d * es);
   if (is16(c.dtype)) {
     o.pmax = take((size_t)rows * slabs * 4);
@@ -273,6 +274,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   float* part = reinterpret_cast<float*>(ws + lay.part);
   const size_t part_cap = partial_bytes(c, total);
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
+  int32_t* slot = reinterpret_cast<int32_t*>(ws + lay.slot);
   void* Hm = ws + lay.Hm;
   const int rows = n_seqs * L;
   const bool bf = is16(c.dtype);
@@ -284,7 +286,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   if (!rope_cs)
     RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta,
                           reinterpret_cast<float*>(ws + lay.rope), s));
-  RUN(launch_head_prep(sp, resp_masked, list, conf_out, argmax_out, s));
+  RUN(launch_head_prep(sp, resp_masked, list, conf_out, argmax_out, slot, s));
   const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
   RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,
                            resp_masked, c.mask_id, c.vocab, d, g0, c.rms_eps, X, A,
@@ -293,6 +295,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   const GemmPlan p_qkv = plan_gemm16(T, 3 * d, d), p_o = plan_gemm16(T, d, d);
   const GemmPlan p_gu = plan_gemm16(T, 2 * F, d), p_dn = plan_gemm16(T, d, F);
   bool a_ready = true;       // A holds RMSNorm(X) for the next GEMM
+  bool hm_ready = false;     // Hm holds the final norm of the masked rows
   for (int l = 0; l < c.n_layers; ++l) {
     const davet_layer_weights& lw = w->layers[l];
     if (!a_ready) RUN(launch_rmsnorm(X, T, d, lw.attn_norm, c.rms_eps,
@@ -328,11 +331,18 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                         nullptr, nullptr, 0, part, part_cap, KC_GEMM_DOWN, s));
       a_ready = false;
       if (p_dn.ksplit > 1) {
-        const bool next = l + 1 < c.n_layers;
-        RUN(launch_reduce_add_norm(dt, part, p_dn.ksplit, T, d, X,
-                                   next ? w->layers[l + 1].attn_norm : nullptr,
-                                   c.rms_eps, next ? A : nullptr, s));
-        a_ready = next;
+        // and the next layer's input norm, or after the last layer the final
+        // norm of the masked rows gathered into Hm
+        if (l + 1 < c.n_layers) {
+          RUN(launch_reduce_add_norm(dt, part, p_dn.ksplit, T, d, X,
+                                     w->layers[l + 1].attn_norm, c.rms_eps, A,
+                                     s));
+          a_ready = true;
+        } else {
+          RUN(launch_reduce_add_gather(dt, part, p_dn.ksplit, T, d, X, sp,
+                                       slot, w->final_norm, c.rms_eps, Hm, s));
+          hm_ready = true;
+        }
       }
     } else {
       RUN(launch_gemm_f32(EPI_STORE, (const float*)A, (const float*)lw.wqkv,
@@ -352,8 +362,9 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
       a_ready = false;
     }
   }
-  RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm, c.rms_eps,
-                               c.dtype, Hm, s));
+  if (!hm_ready)
+    RUN(launch_final_norm_gather(X, sp, list, rows, d, w->final_norm,
+                                 c.rms_eps, c.dtype, Hm, s));
   if (bf) {
     const bool tiled = w->head_layout == DAVET_HEAD_TILED;
     const int live = std::max(1, std::min(rows, rows_bound));
