@@ -165,23 +165,31 @@ struct SeqPack {
 struct ViewPtrs { const void* p[DAVET_MAX_SEQS]; };
 
 // Row kernels
+// The masked response positions of a step (total = n_seqs * L): list[0] =
+// their count, list[1 + j] = the j-th in index order; slot[i] = i's index in
+// the list or -1 (may be null); committed positions get conf = -inf and
+// argmax = -1.
+struct RowList {
+  int total;
+  int32_t* list;
+  float* conf;
+  int32_t* argmax;
+  int32_t* slot;
+};
+// assembly + first norm of every packed row; one extra workgroup builds the
+// masked-row list alongside
 int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const void* embed, const int32_t* prompt_ids,
                          const int32_t* resp_ids, const uint8_t* masked,
                          int mask_id, int vocab, int d, const float* gain,
                          float eps, float* X, void* A, int32_t* pos,
-                         hipStream_t s);
+                         const RowList& rl, hipStream_t s);
 int launch_rmsnorm(const float* X, int rows, int d, const float* gain,
                    float eps, int dtype, void* A, hipStream_t s);
 int launch_rope_table(int max_pos, int head_dim, float theta, float* cs,
                       hipStream_t s);
 int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
                 const SeqPack& sp, const float* cs, hipStream_t s);
-// masked-row list (count in list[0]) and, if slot is given, each response
-// position's index in it (-1: committed)
-int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
-                     float* conf_out, int32_t* argmax_out, int32_t* slot,
-                     hipStream_t s);
 int launch_final_norm_gather(const float* X, const SeqPack& sp,
                              const int32_t* list, int max_rows, int d,
                              const float* gain, float eps, int dtype, void* Hm,

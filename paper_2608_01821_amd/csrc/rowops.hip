@@ -107,7 +107,51 @@ __device__ __forceinline__ void norm_store(float (*x)[8], float ss, int d,
   }
 }
 
+// One workgroup: ordered list of masked response positions (global index
+// s*L + i) with the count in list[0], and (if slot is given) each position's
+// index in that list, -1 for committed ones; committed positions get conf =
+// -inf and argmax = -1.  Each thread takes a contiguous run of positions; the
+// run offsets come from a workgroup prefix sum (wavefront scan + LDS).
+__device__ __forceinline__ void build_row_list(const RowList& rl,
+                                               const uint8_t* __restrict__ masked) {
+  __shared__ int wsum[kThreads / 64];
+  const int total = rl.total;
+  const int per = (total + kThreads - 1) / kThreads;
+  const int lo = min(total, (int)threadIdx.x * per);
+  const int hi = min(total, lo + per);
+  int c = 0;
+  for (int i = lo; i < hi; ++i) c += masked[i] != 0;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int base = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) {
+    if (i < w) base += wsum[i];
+    all += wsum[i];
+  }
+  if (threadIdx.x == 0) rl.list[0] = all;
+  int o = base + incl - c;
+  for (int i = lo; i < hi; ++i) {
+    if (masked[i]) {
+      if (rl.slot) rl.slot[i] = o;
+      rl.list[1 + o++] = i;
+    } else {
+      if (rl.slot) rl.slot[i] = -1;
+      rl.conf[i] = -INFINITY;
+      rl.argmax[i] = -1;
+    }
+  }
+}
+
 // X[row] = [view | E[prompt] | E[resp or mask]] row; A[row] = RMSNorm(X[row]).
+// One extra workgroup after the rows builds the masked-row list meanwhile.
 template <typename Fmt, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
@@ -116,9 +160,13 @@ assemble_norm_kernel(SeqPack sp, ViewPtrs vp, const T* __restrict__ embed,
                      const uint8_t* __restrict__ masked, int mask_id,
                      int vocab, int d, const float* __restrict__ gain,
                      float eps, float* __restrict__ X, T* __restrict__ A,
-                     int32_t* __restrict__ pos) {
+                     int32_t* __restrict__ pos, RowList rl) {
   __shared__ float red[kThreads / 64];
   const int row = blockIdx.x;
+  if (row == sp.total) {
+    build_row_list(rl, masked);
+    return;
+  }
   const int s = find_seq(sp, row);
   const int j = row - sp.row0[s];
   if (threadIdx.x == 0 && pos) pos[row] = j;     // rotary position
@@ -208,50 +256,6 @@ rope_kernel(T* __restrict__ qkv, SeqPack sp, int n_heads, int head_dim,
     const float a = Fmt::load(x[i]), b = Fmt::load(x[i + half]);
     x[i] = Fmt::store(a * c.x - b * c.y);
     x[i + half] = Fmt::store(b * c.x + a * c.y);
-  }
-}
-
-// Single workgroup: ordered list of masked response positions (global index
-// s*L + i) with the count in list[0], and (if slot is given) each position's
-// index in that list, -1 for committed ones; committed positions get conf =
-// -inf and argmax = -1.  Each thread takes a contiguous run of positions; the
-// run offsets come from a workgroup prefix sum (wavefront scan + LDS).
-__global__ void __launch_bounds__(kThreads)
-head_prep_kernel(int total, const uint8_t* __restrict__ masked,
-                 int32_t* __restrict__ list, float* __restrict__ conf_out,
-                 int32_t* __restrict__ argmax_out, int32_t* __restrict__ slot) {
-  __shared__ int wsum[kThreads / 64];
-  const int per = (total + kThreads - 1) / kThreads;
-  const int lo = min(total, (int)threadIdx.x * per);
-  const int hi = min(total, lo + per);
-  int c = 0;
-  for (int i = lo; i < hi; ++i) c += masked[i] != 0;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int incl = c;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) wsum[w] = incl;
-  __syncthreads();
-  int base = 0, all = 0;
-#pragma unroll
-  for (int i = 0; i < kThreads / 64; ++i) {
-    if (i < w) base += wsum[i];
-    all += wsum[i];
-  }
-  if (threadIdx.x == 0) list[0] = all;
-  int o = base + incl - c;
-  for (int i = lo; i < hi; ++i) {
-    if (masked[i]) {
-      if (slot) slot[i] = o;
-      list[1 + o++] = i;
-    } else {
-      if (slot) slot[i] = -1;
-      conf_out[i] = -INFINITY;
-      argmax_out[i] = -1;
-    }
   }
 }
 
@@ -652,12 +656,13 @@ int launch_assemble_norm(const SeqPack& sp, const ViewPtrs& vp, int dtype,
                          const int32_t* resp_ids, const uint8_t* masked,
                          int mask_id, int vocab, int d, const float* gain,
                          float eps, float* X, void* A, int32_t* pos,
-                         hipStream_t s) {
+                         const RowList& rl, hipStream_t s) {
   ProfScope ps(KC_ASSEMBLE, s);
 #define ASM(F)                                                               \
-  hipLaunchKernelGGL(assemble_norm_kernel<F>, dim3(sp.total), dim3(kThreads),  \
-                     0, s, sp, vp, (const F::st*)embed, prompt_ids, resp_ids, \
-                     masked, mask_id, vocab, d, gain, eps, X, (F::st*)A, pos)
+  hipLaunchKernelGGL(assemble_norm_kernel<F>, dim3(sp.total + 1),             \
+                     dim3(kThreads), 0, s, sp, vp, (const F::st*)embed,       \
+                     prompt_ids, resp_ids, masked, mask_id, vocab, d, gain,   \
+                     eps, X, (F::st*)A, pos, rl)
   if (dtype == DAVET_BF16) ASM(BF16S);
   else if (dtype == DAVET_F16) ASM(F16S);
   else ASM(F32S);
@@ -700,17 +705,6 @@ int launch_rope(void* qkv, int rows, int n_heads, int head_dim, int dtype,
   else if (dtype == DAVET_F16) ROPE(F16S);
   else ROPE(F32S);
 #undef ROPE
-  DAVET_HIP(hipGetLastError());
-  return DAVET_OK;
-}
-
-int launch_head_prep(const SeqPack& sp, const uint8_t* masked, int32_t* list,
-                     float* conf_out, int32_t* argmax_out, int32_t* slot,
-                     hipStream_t s) {
-  ProfScope ps(KC_HEAD_PREP, s);
-  hipLaunchKernelGGL(head_prep_kernel, dim3(1), dim3(kThreads), 0, s,
-                     sp.n_seqs * sp.L, masked, list, conf_out, argmax_out,
-                     slot);
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }

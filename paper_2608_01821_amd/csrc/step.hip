@@ -286,11 +286,11 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   if (!rope_cs)
     RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta,
                           reinterpret_cast<float*>(ws + lay.rope), s));
-  RUN(launch_head_prep(sp, resp_masked, list, conf_out, argmax_out, slot, s));
   const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
+  const RowList rl{n_seqs * L, list, conf_out, argmax_out, slot};
   RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,
                            resp_masked, c.mask_id, c.vocab, d, g0, c.rms_eps, X, A,
-                           pos, s));
+                           pos, rl, s));
   const int T = sp.total;
   const GemmPlan p_qkv = plan_gemm16(T, 3 * d, d), p_o = plan_gemm16(T, d, d);
   const GemmPlan p_gu = plan_gemm16(T, 2 * F, d), p_dn = plan_gemm16(T, d, F);
