@@ -44,22 +44,24 @@ def test_pack_head_matches_formula(vocab, d):
 # (config, sequences, response length, masked fraction): the last three pack
 # 200, 300 and 500 response rows, so the head runs its 256 x 256 tile over one
 # and two row slots and its 128 x 256 tile over three
-@pytest.mark.parametrize("cid,n_seqs,L,frac", [
-    (11, 3, None, 0.6), (12, 3, None, 0.6), (12, 5, 40, 1.0),
-    (12, 6, 50, 0.9), (12, 5, 100, 0.8)])
-def test_tiled_head_step(cid, n_seqs, L, frac):
+@pytest.mark.parametrize("cid,n_seqs,L,frac,mode", [
+    (11, 3, None, 0.6, "f16"), (12, 3, None, 0.6, "f16"),
+    (12, 5, 40, 1.0, "f16"), (12, 6, 50, 0.9, "f16"),
+    (12, 5, 100, 0.8, "f16"), (12, 5, 100, 0.8, "bf16")])
+def test_tiled_head_step(cid, n_seqs, L, frac, mode):
     import dataclasses
     cfg = synth.get_any_config(cid)
     if L is not None:
         cfg = dataclasses.replace(cfg, resp_len=L, n_seqs=n_seqs)
-    mdl = Model(cfg)
+    mdl = Model(cfg, mode)
     s = synth.gen_sample(cfg)
     n_seqs = min(cfg.n_seqs, n_seqs)
-    samples = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i])
-               for i in range(n_seqs)]
+    samples = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i],
+                      mode) for i in range(n_seqs)]
     tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
                         dtype=torch.int16, device="cuda")
-    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d, dv.DAVET_F16)
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d,
+                       dv.DAVET_F16 if mode == "f16" else dv.DAVET_BF16)
     w_tiled = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
                          head_layout=dv.DAVET_HEAD_TILED)
     rng = np.random.default_rng(cid)
@@ -76,14 +78,14 @@ def test_tiled_head_step(cid, n_seqs, L, frac):
     total = sum(nview) + int(cu[-1]) + n_seqs * L
     outs = []
     for w in (mdl.weights, w_tiled):
-        ws = workspace(cfg, total, n_seqs, L)
+        ws = workspace(cfg, total, n_seqs, L, mode)
         d_ids = torch.from_numpy(ids.astype(np.int32)).cuda()
         d_m = torch.from_numpy(masked.astype(np.uint8)).cuda()
         conf = torch.empty(n_seqs * L, device="cuda")
         am = torch.empty(n_seqs * L, dtype=torch.int32, device="cuda")
         lg = torch.full((n_seqs * L, cfg.vocab), 55.0, device="cuda")
-        dv.davet_denoise_step(model_cfg(cfg), w, views_, nview, prompt, cu,
-                              d_ids, d_m, L, conf, am, lg, ws)
+        dv.davet_denoise_step(model_cfg(cfg, mode), w, views_, nview, prompt,
+                              cu, d_ids, d_m, L, conf, am, lg, ws)
         torch.cuda.synchronize()
         outs.append((conf.cpu().numpy(), am.cpu().numpy(), lg.cpu().numpy()))
     (c0, a0, l0), (c1, a1, l1) = outs

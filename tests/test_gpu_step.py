@@ -73,3 +73,22 @@ def test_ragged_batch_step(cid, mode):
                                       masked[i])
         compare(cfg, TOL[mode], masked[i], g_conf[i], g_am[i], g_lg[i],
                 pos, lg, am, cf)
+
+
+@pytest.mark.parametrize("cid,mode", [(11, "f16"), (11, "bf16"), (1, "f32")])
+def test_step_without_layers(cid, mode):
+    """No transformer layers: the step is the final norm of the embedded
+    masked rows and the vocabulary head, so the final norm and gather run on
+    their own (there is no last-layer split-K reduction to carry them)."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_any_config(cid), n_layers=0)
+    mdl = Model(cfg, mode)
+    s = synth.gen_sample(cfg)
+    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0],
+                    mode)
+    rng = np.random.default_rng(21)
+    ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.6)
+    g_conf, g_am, g_lg = run_gpu_step(cfg, mdl, [sample], [1], ids, masked)
+    pos, lg, am, cf = oracle_step(cfg, mdl, sample, 1, ids, masked)
+    compare(cfg, TOL[mdl.mode], masked, g_conf[0], g_am[0], g_lg[0], pos, lg,
+            am, cf)
