@@ -592,10 +592,11 @@ int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
       case 2: { constexpr int KS = 2; BODY; } break;                        \
       case 3: { constexpr int KS = 3; BODY; } break;                        \
       case 4: { constexpr int KS = 4; BODY; } break;                        \
+      case 5: { constexpr int KS = 5; BODY; } break;                        \
       case 6: { constexpr int KS = 6; BODY; } break;                        \
       case 8: { constexpr int KS = 8; BODY; } break;                        \
       default: return set_error(DAVET_EINVAL,                              \
-                                "split-K: ksplit must be 2, 3, 4, 6 or 8"); \
+                                "split-K: ksplit must be 2, 3, 4, 5, 6 or 8"); \
     }                                                                       \
   } while (0)
 
