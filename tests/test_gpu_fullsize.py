@@ -104,7 +104,10 @@ def test_one_layer_full_size(one_layer, level, frac):
 
 def test_ragged16_full_size():
     """The 16-sequence ragged batch in one packed call; four sequences are
-    checked against the oracle, each on its own."""
+    checked against the oracle, each on its own.  Then the same call with the
+    tiled head (davet_pack_head, as the benchmark runs it: over ~1600 masked
+    rows its 256 x 256 tile) gives the same argmaxes and logits bit for bit
+    and the same confidences up to the regrouping of the softmax sum."""
     cfg = synth.get_config(5)
     say("generating config 5")
     mdl = Model(cfg)
@@ -121,6 +124,20 @@ def test_ragged16_full_size():
     for i in (0, 5, 10, 15):
         check_sampled(cfg, mdl, samples[i], levels[i], ids[i], masked[i],
                       g_conf[i], g_am[i], g_lg[i], 6, 100 + i)
+    tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
+                        dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d,
+                       dv.DAVET_F16 if mdl.mode == "f16" else dv.DAVET_BF16)
+    row_w = mdl.weights
+    mdl.weights = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
+                             head_layout=dv.DAVET_HEAD_TILED)
+    try:
+        t_conf, t_am, t_lg = gpu_step(cfg, mdl, samples, levels, ids, masked)
+    finally:
+        mdl.weights = row_w
+    assert np.array_equal(t_am, g_am)
+    assert_conf_regrouped(t_conf, g_conf)
+    assert bool(torch.equal(t_lg, g_lg))
 
 
 def test_stack32_full_size_low_view():
