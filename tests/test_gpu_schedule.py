@@ -64,7 +64,7 @@ def test_teacher_forced_loop(cid):
         assert np.array_equal(d_m.cpu().numpy(), masked)
 
 
-def _run_schedule(cfg, mdl, s, pols=None, fixed=None):
+def _run_schedule(cfg, mdl, s, pols=None, fixed=None, weights=None):
     n = cfg.n_seqs
     L, T = cfg.resp_len, cfg.steps
     mode = mdl.mode
@@ -83,7 +83,8 @@ def _run_schedule(cfg, mdl, s, pols=None, fixed=None):
     ctr = torch.empty((T, n * L), device="cuda")
     atr = torch.empty((T, n * L), dtype=torch.int32, device="cuda")
     levels, budgets = dv.davet_run_schedule(
-        model_cfg(cfg, mode), mdl.weights, geoms, visual, bufs, prompt, cu, L, T,
+        model_cfg(cfg, mode), weights or mdl.weights, geoms, visual, bufs,
+        prompt, cu, L, T,
         cfg.k, pols, fixed, ids, msk, ws, ctr, atr)
     torch.cuda.synchronize()
     return (np.array(levels).reshape(n, T), np.array(budgets).reshape(n, T),
@@ -220,6 +221,46 @@ def test_run_schedule_head_over_several_row_tiles():
     lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
     _check_invariants(cfg, ctr, atr, ids, msk)
     assert cfg.n_seqs * cfg.resp_len > 3 * 128
+    for i, pol in enumerate(pols):
+        ref = loop.run_sequence(cfg, mdl.host,
+                                to_mode(s["visual"][i], mdl.mode)[1],
+                                s["n_crops"][i], s["prompts"][i], cfg.steps,
+                                cfg.k, pol=p, demand=dv.davet_demand_prior(
+                                    s["categories"][i]), out_dtype=mdl.mode)
+        assert ref["trace"]["levels"][0] == lv[i, 0]
+        assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
+                                        i) >= 1
+
+
+def test_run_schedule_tiled_head():
+    """The loop as the benchmark runs it, with the head packed by
+    davet_pack_head: 500, 300 and 100 masked rows over three steps (the head's
+    256 x 256 tile, then its 128 x 256 tile over three and one row slots).
+    Step 1 sees identical inputs in both layouts: the same argmaxes and
+    confidences up to the regrouping of the softmax sum; the tiled run keeps
+    every invariant and matches the oracle as the row-major run does."""
+    import dataclasses
+    from gpu_util import assert_conf_regrouped
+    cfg = dataclasses.replace(synth.get_any_config(12), resp_len=100, k=40,
+                              steps=3)
+    mdl = Model(cfg)
+    tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
+                        dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d,
+                       dv.DAVET_F16 if mdl.mode == "f16" else dv.DAVET_BF16)
+    w_tiled = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
+                         head_layout=dv.DAVET_HEAD_TILED)
+    s = synth.gen_sample(cfg)
+    p = cfg.policy
+    pols = [dv.Policy(p["B"], p["rho"], p["alpha"], dv.davet_demand_prior(c),
+                      1 if p["early"] else 0, cfg.K) for c in s["categories"]]
+    lv_r, _, ctr_r, atr_r, _, _ = _run_schedule(cfg, mdl, s, pols=pols)
+    lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols,
+                                               weights=w_tiled)
+    _check_invariants(cfg, ctr, atr, ids, msk)
+    assert np.array_equal(lv[:, 0], lv_r[:, 0])
+    assert np.array_equal(atr[0], atr_r[0])
+    assert_conf_regrouped(ctr[0], ctr_r[0])
     for i, pol in enumerate(pols):
         ref = loop.run_sequence(cfg, mdl.host,
                                 to_mode(s["visual"][i], mdl.mode)[1],
