@@ -122,7 +122,10 @@ typedef struct davet_layer_weights {
   const float* ffn_norm;
 } davet_layer_weights;
 
-/* Layout of the vocabulary-head weights (davet_weights.head_layout). */
+/* Layout of the vocabulary-head weights (davet_weights.head_layout).  Both
+ * layouts give the same logits and argmaxes bit for bit; the confidences may
+ * differ in their last bits (the tiled head sums the exponentials over
+ * 256-column vocabulary slabs, the row-major one over 128-column slabs). */
 typedef enum davet_head_layout {
   DAVET_HEAD_ROWS = 0,   /* [vocab, d] row-major */
   DAVET_HEAD_TILED = 1   /* 16-bit models only: the output of davet_pack_head */
