@@ -7,11 +7,15 @@
 // order (a sequential sum over positions in index order), no contraction
 // into fused multiply-adds, IEEE-rounded division.
 //
-// One wavefront per sample: the lanes stage the sample's confidences, flags
-// and predictions in LDS with coalesced loads, lane 0 runs the ordered sum
-// and the policy arithmetic.  The outputs may live in pinned host memory
-// (the schedule loop reads the next levels from there without a copy, and
-// polls a completion stamp instead of a stream synchronisation).
+// One wavefront per sample: the lanes stage each position's contribution to
+// the sum in LDS with coalesced loads (its confidence as a double where the
+// position is still masked, +0.0 elsewhere: the running sum starts at +0.0
+// and x + 0.0 == x for every x it can take, so this is the masked-only sum
+// bit for bit) and count the masked and changed positions with wavefront
+// sums; lane 0 runs the ordered sum, branch-free so its LDS reads pipeline,
+// and the policy arithmetic.  The outputs may live in pinned host memory (the
+// schedule loop reads the next levels from there without a copy, and polls a
+// completion stamp instead of a stream synchronisation).
 
 #include "common.h"
 
@@ -39,30 +43,28 @@ policy_step_kernel(int n_seqs, int L, int K, const float* __restrict__ conf,
                    double* cbar_out, double* churn_out, int32_t* done,
                    int32_t stamp) {
 #pragma clang fp contract(off)
-  __shared__ float s_conf[POL_WAVES][DAVET_MAX_RESP];
-  __shared__ uint8_t s_flag[POL_WAVES][DAVET_MAX_RESP];  // bit0 masked, bit1 changed
+  __shared__ double s_term[POL_WAVES][DAVET_MAX_RESP];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int s = w; s < n_seqs; s += POL_WAVES) {
     const size_t o = (size_t)s * L;
+    int n = 0, changed = 0;
     for (int i = lane; i < L; i += 64) {
-      const uint8_t m = masked_after[o + i] ? 1 : 0;
-      const uint8_t ch =
-          (argmax_prev && argmax[o + i] != argmax_prev[o + i]) ? 2 : 0;
-      s_flag[w][i] = m | ch;
-      s_conf[w][i] = conf[o + i];
+      const bool m = masked_after[o + i] != 0;
+      s_term[w][i] = m ? (double)conf[o + i] : 0.0;
+      n += m;
+      changed += m && argmax_prev && argmax[o + i] != argmax_prev[o + i];
+    }
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) {
+      n += __shfl_xor(n, d, 64);
+      changed += __shfl_xor(changed, d, 64);
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     if (lane == 0) {
       double sum = 0.0;
-      int n = 0, changed = 0;
-      for (int i = 0; i < L; ++i) {
-        const uint8_t f = s_flag[w][i];
-        if (!(f & 1)) continue;
-        sum = sum + (double)s_conf[w][i];
-        ++n;
-        if (f & 2) ++changed;
-      }
+#pragma unroll 16
+      for (int i = 0; i < L; ++i) sum = sum + s_term[w][i];
       const double cbar = n ? sum / (double)n : 0.0;
       const double churn =
           (n && argmax_prev) ? (double)changed / (double)n : 0.0;
