@@ -119,3 +119,56 @@ def test_tiled_head_rejected_for_fp32():
                               [smp.sizes[-1]], smp.dev_prompt,
                               [0, len(smp.prompt)], d_ids, d_m, L, conf, am,
                               None, ws)
+
+
+@pytest.mark.parametrize("n_seqs,L", [(64, 16), (1, 1024), (64, 1024)])
+def test_step_at_maximum_shapes(n_seqs, L):
+    """The packed step at the limits the C ABI accepts (64 sequences, 1024
+    response positions each, 65536 response rows at most): the first, a
+    middle and the last sequence against the oracle, and the tiled head
+    (256 x 256 tiles over up to 256 row slots) against the row-major one."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_any_config(12), resp_len=L,
+                              n_seqs=n_seqs)
+    mdl = Model(cfg)
+    s = synth.gen_sample(cfg)
+    samples = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i])
+               for i in range(n_seqs)]
+    tiled = torch.empty(dv.davet_head_tiled_elems(cfg.vocab, cfg.d),
+                        dtype=torch.int16, device="cuda")
+    dv.davet_pack_head(mdl.dev_head, tiled, cfg.vocab, cfg.d, dv.DAVET_F16)
+    w_tiled = dv.Weights(mdl.dev_embed, tiled, mdl.dev_layers,
+                         head_layout=dv.DAVET_HEAD_TILED)
+    rng = np.random.default_rng(n_seqs + L)
+    st = [random_state(rng, L, cfg.mask_id, cfg.vocab, 0.9) for _ in samples]
+    ids = np.stack([a for a, _ in st])
+    masked = np.stack([b for _, b in st])
+    levels = [i % cfg.K for i in range(n_seqs)]
+    prompt = torch.cat([x.dev_prompt for x in samples])
+    cu = np.concatenate([[0], np.cumsum([len(x.prompt) for x in samples])])
+    views_ = [x.dev_levels[lv] for x, lv in zip(samples, levels)]
+    nview = [x.sizes[lv] for x, lv in zip(samples, levels)]
+    total = sum(nview) + int(cu[-1]) + n_seqs * L
+    ws = workspace(cfg, total, n_seqs, L)
+    outs = []
+    for w in (mdl.weights, w_tiled):
+        d_ids = torch.from_numpy(ids.astype(np.int32)).cuda()
+        d_m = torch.from_numpy(masked.astype(np.uint8)).cuda()
+        conf = torch.empty(n_seqs * L, device="cuda")
+        am = torch.empty(n_seqs * L, dtype=torch.int32, device="cuda")
+        lg = torch.full((n_seqs * L, cfg.vocab), 55.0, device="cuda")
+        dv.davet_denoise_step(model_cfg(cfg), w, views_, nview, prompt, cu,
+                              d_ids, d_m, L, conf, am, lg, ws)
+        torch.cuda.synchronize()
+        outs.append((conf.cpu().numpy(), am.cpu().numpy(), lg))
+    (c0, a0, l0), (c1, a1, l1) = outs
+    assert np.array_equal(a0, a1)
+    assert_conf_regrouped(c1, c0)
+    assert bool(torch.equal(l0, l1))
+    l0 = l0.cpu().numpy()
+    for i in sorted({0, n_seqs // 2, n_seqs - 1}):
+        pos, rl, ra, rc = oracle_step(cfg, mdl, samples[i], levels[i], ids[i],
+                                      masked[i])
+        sl = slice(i * L, (i + 1) * L)
+        compare(cfg, TOL[mdl.mode], masked[i], c0[sl], a0[sl],
+                l0[sl].reshape(L, cfg.vocab), pos, rl, ra, rc)
