@@ -270,3 +270,29 @@ def test_run_schedule_tiled_head():
         assert ref["trace"]["levels"][0] == lv[i, 0]
         assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
                                         i) >= 1
+
+
+def test_run_schedule_64_sequences():
+    """The policy loop over 64 sequences, the most the C ABI takes (the
+    device policy step serves four per wavefront, the pinned mailbox holds
+    64 levels): every invariant on every sequence, and three sequences
+    against the oracle's own trajectory."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_any_config(12), n_seqs=64,
+                              resp_len=32, k=8, steps=3)
+    mdl = Model(cfg)
+    s = synth.gen_sample(cfg)
+    p = cfg.policy
+    pols = [dv.Policy(p["B"], p["rho"], p["alpha"], dv.davet_demand_prior(c),
+                      1 if p["early"] else 0, cfg.K) for c in s["categories"]]
+    lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
+    _check_invariants(cfg, ctr, atr, ids, msk)
+    for i in (0, 31, 63):
+        ref = loop.run_sequence(cfg, mdl.host,
+                                to_mode(s["visual"][i], mdl.mode)[1],
+                                s["n_crops"][i], s["prompts"][i], cfg.steps,
+                                cfg.k, pol=p, demand=dv.davet_demand_prior(
+                                    s["categories"][i]), out_dtype=mdl.mode)
+        assert ref["trace"]["levels"][0] == lv[i, 0]
+        assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
+                                        i) >= 1
