@@ -92,3 +92,46 @@ def test_step_without_layers(cid, mode):
     pos, lg, am, cf = oracle_step(cfg, mdl, sample, 1, ids, masked)
     compare(cfg, TOL[mdl.mode], masked, g_conf[0], g_am[0], g_lg[0], pos, lg,
             am, cf)
+
+
+def test_step_edge_inputs():
+    """Edge inputs in one packed call: a sequence with neither view tokens
+    nor prompt (only its response), one with a view but no prompt, one with
+    every position already committed (conf -inf, argmax -1, logit rows
+    untouched), next to an ordinary one; each against its own oracle run."""
+    import copy
+    cfg = synth.get_any_config(12)
+    mdl = Model(cfg)
+    s = synth.gen_sample(cfg)
+    base = [Sample(cfg, s["n_crops"][i], s["visual"][i], s["prompts"][i])
+            for i in range(4)]
+    L = cfg.resp_len
+    empty_prompt = np.zeros(0, np.int32)
+
+    def without(smp, view=False, prompt=False):
+        x = copy.copy(smp)
+        if view:
+            x.sizes = [0] + list(smp.sizes[1:])
+            x.dev_levels = [smp.dev_levels[0][:0]] + list(smp.dev_levels[1:])
+            x.ref_levels = [smp.ref_levels[0][:0]] + list(smp.ref_levels[1:])
+        if prompt:
+            x.prompt = empty_prompt
+            x.dev_prompt = torch.from_numpy(empty_prompt).cuda()
+        return x
+    samples = [without(base[0], view=True, prompt=True),
+               without(base[1], prompt=True), base[2], base[3]]
+    levels = [0, 1, 2, 0]
+    rng = np.random.default_rng(77)
+    st = [random_state(rng, L, cfg.mask_id, cfg.vocab, 0.7) for _ in range(4)]
+    ids = np.stack([a for a, _ in st])
+    masked = np.stack([b for _, b in st])
+    masked[2] = 0                              # nothing left to denoise
+    ids[2] = rng.integers(0, cfg.vocab - 1, L)
+    g_conf, g_am, g_lg = run_gpu_step(cfg, mdl, samples, levels, ids, masked)
+    assert np.all(g_conf[2] == -np.inf) and np.all(g_am[2] == -1)
+    assert np.all(g_lg[2] == 55.0)
+    for i in (0, 1, 3):
+        pos, lg, am, cf = oracle_step(cfg, mdl, samples[i], levels[i], ids[i],
+                                      masked[i])
+        compare(cfg, TOL[mdl.mode], masked[i], g_conf[i], g_am[i], g_lg[i],
+                pos, lg, am, cf)
