@@ -187,3 +187,150 @@ def test_step_flops_closed_form():
     per_layer = 2 * 889 * (4 * 4096 ** 2 + 3 * 4096 * 12288) \
         + 4 * 889 ** 2 * 4096
     assert f == per_layer + 2 * 128 * 4096 * 126464
+
+
+def _torch_layer_gains(x, w, H, D, eps, theta):
+    """_torch_layer with the RMSNorm gains of the layer (attn_norm, ffn_norm)
+    passed to torch's rms_norm as its weight."""
+    N, d = x.shape
+    xt = _t(x)
+    a = F.rms_norm(xt, (d,), _t(w["attn_norm"]), eps=eps)
+    qkv = a @ _t(w["wqkv"]).T
+    q = _rope_complex(qkv[:, :d].reshape(N, H, D).numpy(), theta)
+    k = _rope_complex(qkv[:, d:2 * d].reshape(N, H, D).numpy(), theta)
+    v = qkv[:, 2 * d:].reshape(N, H, D)
+    o = F.scaled_dot_product_attention(
+        _t(q).transpose(0, 1), _t(k).transpose(0, 1), v.transpose(0, 1))
+    xt = xt + o.transpose(0, 1).reshape(N, d) @ _t(w["wo"]).T
+    a = F.rms_norm(xt, (d,), _t(w["ffn_norm"]), eps=eps)
+    hdn = F.silu(a @ _t(w["wg"]).T) * (a @ _t(w["wu"]).T)
+    return (xt + hdn @ _t(w["wd"]).T).numpy()
+
+
+def _torch_step(view, prompt, resp, masked, W, H, D, eps, theta, mask_id,
+                rows, row_offset=None, final_norm=True):
+    """Eq. (1) at the response positions ``rows`` composed from torch float64
+    pieces: F.embedding for the prompt and the response (the [MASK] id where
+    masked), the layer above per layer, torch's rms_norm with the final gain
+    on the hidden states of the response rows, then the head product.
+    ``row_offset`` (default: the first response row, N - L) and
+    ``final_norm`` exist so that the test can show a misplaced gather or a
+    dropped final norm is caught."""
+    E = _t(W["embed"])
+    tok = torch.where(torch.from_numpy(np.asarray(masked, bool)),
+                      torch.tensor(mask_id),
+                      torch.from_numpy(np.asarray(resp, np.int64)))
+    x = torch.cat([_t(view),
+                   F.embedding(torch.from_numpy(np.asarray(prompt, np.int64)),
+                               E),
+                   F.embedding(tok, E)], dim=0).numpy()
+    for w in W["layers"]:
+        x = _torch_layer_gains(x, w, H, D, eps, theta)
+    n, d = x.shape
+    off = n - len(resp) if row_offset is None else row_offset
+    h = _t(x)[off + torch.from_numpy(np.asarray(rows, np.int64))]
+    if final_norm:
+        h = F.rms_norm(h, (d,), _t(W["final_norm"]), eps=eps)
+    return (h @ _t(W["head"]).T).numpy()
+
+
+def _tiny_model(rng, n_layers, d, Fh, V):
+    def mat(r, c, s=0.15):
+        return rng.standard_normal((r, c)) * s
+
+    layers = [dict(wqkv=mat(3 * d, d), wo=mat(d, d), wg=mat(Fh, d),
+                   wu=mat(Fh, d), wd=mat(d, Fh),
+                   attn_norm=1.0 + 0.3 * rng.standard_normal(d),
+                   ffn_norm=1.0 + 0.3 * rng.standard_normal(d))
+              for _ in range(n_layers)]
+    return dict(embed=mat(V, d, 1.0), head=mat(V, d, 0.5), layers=layers,
+                final_norm=1.0 + 0.3 * rng.standard_normal(d))
+
+
+class _Cfg:
+    n_layers, n_heads, head_dim = 2, 2, 16
+    rms_eps, rope_theta, mask_id = 1e-5, 100.0, 40
+
+
+def test_step_logits_against_torch_composition():
+    """The oracle's whole step (sequence layout, rotary positions over the
+    full sequence, layer stack, gather of the response rows, final norm,
+    head) against an independent composition of torch float64 pieces, on a
+    2-layer model with a view, a prompt and a partially committed response;
+    once at every masked position, once at an explicit subset of rows that
+    includes committed positions."""
+    rng = np.random.default_rng(11)
+    c = _Cfg()
+    d, Fh, V = c.n_heads * c.head_dim, 48, c.mask_id + 1
+    W = _tiny_model(rng, c.n_layers, d, Fh, V)
+    view = rng.standard_normal((5, d))
+    prompt = rng.integers(0, V - 1, 4)
+    L = 7
+    masked = np.array([1, 0, 1, 1, 0, 0, 1], np.uint8)
+    resp = rng.integers(0, V - 1, L)
+    resp[masked == 1] = c.mask_id
+
+    pos, got = model.step_logits(c, view, prompt, resp, masked, W)
+    np.testing.assert_array_equal(pos, np.nonzero(masked)[0])
+    ref = _torch_step(view, prompt, resp, masked, W, c.n_heads, c.head_dim,
+                      c.rms_eps, c.rope_theta, c.mask_id, pos)
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+    rows = np.array([0, 1, 4, 6])
+    pos2, got2 = model.step_logits(c, view, prompt, resp, masked, W,
+                                   rows=rows)
+    np.testing.assert_array_equal(pos2, rows)
+    ref2 = _torch_step(view, prompt, resp, masked, W, c.n_heads, c.head_dim,
+                       c.rms_eps, c.rope_theta, c.mask_id, rows)
+    np.testing.assert_allclose(got2, ref2, rtol=1e-11, atol=1e-11)
+
+    # the comparison is sharp enough to catch the plausible slips: gathering
+    # hidden[pos] instead of hidden[N - L + pos], dropping the final norm,
+    # embedding the committed id at a masked position
+    bad_off = _torch_step(view, prompt, resp, masked, W, c.n_heads,
+                          c.head_dim, c.rms_eps, c.rope_theta, c.mask_id,
+                          pos, row_offset=0)
+    assert np.abs(bad_off - got).max() > 1e-2
+    no_norm = _torch_step(view, prompt, resp, masked, W, c.n_heads,
+                          c.head_dim, c.rms_eps, c.rope_theta, c.mask_id,
+                          pos, final_norm=False)
+    assert np.abs(no_norm - got).max() > 1e-2
+    resp_leak = resp.copy()
+    resp_leak[0] = 3
+    leak = _torch_step(view, prompt, resp_leak, np.zeros(L, np.uint8), W,
+                       c.n_heads, c.head_dim, c.rms_eps, c.rope_theta,
+                       c.mask_id, pos)
+    assert np.abs(leak - got).max() > 1e-2
+
+
+def test_step_logits_rotary_positions_span_whole_sequence():
+    """Rotary positions run 0..N-1 over [view | prompt | response]: moving a
+    token from the prompt into the view (same rows, same order) changes
+    nothing, while restarting positions at the prompt (a plausible slip)
+    changes the logits; checked against the torch composition, whose rotary
+    table always has N rows."""
+    rng = np.random.default_rng(12)
+    c = _Cfg()
+    d, Fh, V = c.n_heads * c.head_dim, 48, c.mask_id + 1
+    W = _tiny_model(rng, c.n_layers, d, Fh, V)
+    prompt = rng.integers(0, V - 1, 3)
+    view = rng.standard_normal((4, d))
+    L = 5
+    masked = np.ones(L, np.uint8)
+    resp = np.full(L, c.mask_id)
+    _, base = model.step_logits(c, view, prompt, resp, masked, W)
+    # the same rows with the first prompt token given as a view row
+    view2 = np.concatenate([view, np.asarray(W["embed"])[prompt[:1]]])
+    _, moved = model.step_logits(c, view2, prompt[1:], resp, masked, W)
+    np.testing.assert_allclose(moved, base, rtol=1e-12, atol=1e-12)
+    # positions restarted after the view: compose the two parts by hand
+    E = np.asarray(W["embed"])
+    x = np.concatenate([view, E[prompt], E[resp]])
+    N = x.shape[0]
+    ang = model.rope_angles(N, c.head_dim, c.rope_theta)
+    ang_restart = np.concatenate([ang[:4], ang[:N - 4]])
+    for w in W["layers"]:
+        x = model.layer(x, w, c.n_heads, c.head_dim, c.rms_eps, ang_restart)
+    h = model.rmsnorm(x[N - L:], W["final_norm"], c.rms_eps)
+    wrong = h @ np.asarray(W["head"]).T
+    assert np.abs(wrong - base).max() > 1e-2
