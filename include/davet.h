@@ -20,8 +20,9 @@
  *   - Pointers are DEVICE pointers unless the comment says host.  Arrays are
  *     dense and row-major.  The caller owns every buffer, including the
  *     workspace; the library never frees caller memory and allocates no device
- *     memory (davet_run_schedule may use small host-side vectors and, in
- *     policy mode, a few hundred bytes of pinned host memory per call).
+ *     memory (davet_run_schedule uses small host-side vectors; its policy
+ *     mode writes into a caller-owned mailbox made once by
+ *     davet_mailbox_create).
  *   - Device work is enqueued asynchronously on the given HIP stream.  Only
  *     davet_run_schedule in policy mode synchronises: once per step, on the
  *     GPU kernel that writes the next levels (the next step's launch sizes
@@ -33,10 +34,17 @@
  *     patterns, DAVET_F16 = IEEE binary16 bit patterns (both uint16).  The
  *     16-bit modes feed 16-bit operands of that type to the matrix cores with
  *     float32 accumulation; residual streams, softmax statistics and norms
- *     run in float32 in every mode.  A bf16 model runs in either 16-bit
- *     mode: its weights convert to fp16 exactly (davet_convert) whenever
- *     |w| >= 2^-17, and fp16 operands carry 3 more mantissa bits through
- *     the activations at the same matrix-core rate.
+ *     run in float32 in every mode.  A bf16 model is meant to run in the
+ *     DAVET_F16 mode: davet_convert rounds its weights to fp16 (a bf16 value
+ *     converts exactly when 2^-17 <= |w| <= 65504; smaller ones fall into
+ *     fp16's subnormal range and lose bits, |w| <= 2^-25 becomes zero), and
+ *     fp16 operands carry 3 more mantissa
+ *     bits through the activations at the same matrix-core rate.  The
+ *     DAVET_BF16 mode (bf16 activations into the matrix cores) is accurate
+ *     to logits rel-RMS <= 1e-2 against a float64 evaluation only for
+ *     shallow stacks: measured 6e-3 for one 8B-shaped layer and 2.2e-2 for
+ *     32 layers, whose error exceeds that bound; use DAVET_F16 for deep
+ *     stacks.
  */
 #ifndef DAVET_H
 #define DAVET_H
@@ -252,8 +260,8 @@ int davet_realizer_maps(const davet_view_geom* g, const double* keys,
                         int32_t* const* idx_members, hipStream_t stream);
 
 /* Element-type conversion of n values, rounding to nearest even (e.g. a bf16
- * checkpoint into the fp16 operand mode: exact whenever |x| >= 2^-17 and
- * |x| <= 65504).  src and dst are device buffers of n elements of their
+ * checkpoint into the fp16 operand mode: a bf16 value converts exactly when
+ * 2^-17 <= |x| <= 65504, smaller ones lose bits in fp16's subnormal range).  src and dst are device buffers of n elements of their
  * dtypes and must not overlap.  Errors: EINVAL (null, overlap), EDTYPE. */
 int davet_convert(const void* src, int32_t src_dtype, void* dst,
                   int32_t dst_dtype, size_t n, hipStream_t stream);
@@ -395,15 +403,37 @@ int davet_policy_step_device(int32_t n_seqs, int32_t L, int32_t t, int32_t T,
 
 /* ------------------------------------------------------------- schedule -- */
 
+/* Mailbox of the policy-mode loop (Sec. 4.2's closed loop): after every
+ * step the GPU writes the next levels and budgets of each sample into it,
+ * then a stamp the host waits for.  davet_mailbox_create is a one-time
+ * set-up call: it allocates a few hundred bytes of pinned, host-coherent
+ * memory (hipHostMalloc) that the caller owns until davet_mailbox_destroy,
+ * which first synchronises the device (a policy step still queued may write
+ * the mailbox) and then frees it.  A mailbox serves one davet_run_schedule
+ * call at a time (calls that overlap on one mailbox race); each call uses
+ * stamps no earlier call on that mailbox used.  Host only.
+ * Errors: EINVAL (null out), ENOMEM, EHIP. */
+typedef struct davet_mailbox davet_mailbox;
+int davet_mailbox_create(davet_mailbox** out /*host*/);
+int davet_mailbox_destroy(davet_mailbox* mailbox);   /* NULL: no-op */
+
+/* Host-side limit (seconds, default 120) on each wait of davet_run_schedule
+ * for a step's published levels; a longer wait returns DAVET_EHIP while the
+ * stream may still be running (synchronise it before reusing the mailbox,
+ * the workspace or the outputs).  Process-wide.  Errors: EINVAL (not
+ * positive and finite). */
+int davet_set_wait_limit(double seconds);
+
 /* The whole DAVET loop for a packed batch (Sec. 3.1 and Sec. 4; Fig. 2):
  * davet_build_views once per sequence into view_bufs, then for t = 1..T:
  * choose each sequence's level -- fixed_levels[s*T + t-1] when fixed_levels is
  * given, else the policy pols[s] (Eqs. 7-9) from the signals of step t-1 --
- * davet_denoise_step, davet_unmask with k.  In policy mode each step ends with
- * the device policy step (as davet_policy_step_device, writing the next
- * levels and budgets to pinned host memory) and a stream synchronisation;
- * the levels and budgets equal those of davet_step_stats + davet_policy_step
- * on the same signals bit for bit.
+ * davet_denoise_step, davet_unmask with k.  In policy mode each step but the
+ * last ends with the device policy step (as davet_policy_step_device,
+ * writing the next levels and budgets into the mailbox) and a host wait for
+ * its stamp, bounded by davet_set_wait_limit; the levels and budgets equal
+ * those of davet_step_stats + davet_policy_step on the same signals bit for
+ * bit.  The call allocates and frees no host or device memory.
  *   geoms: HOST [n_seqs] (d and dtype must match cfg)
  *   visual: HOST [n_seqs] device pointers to each v
  *   view_bufs: HOST [n_seqs*(K-1)] device pointers, pooled level l of
@@ -416,7 +446,11 @@ int davet_policy_step_device(int32_t n_seqs, int32_t L, int32_t t, int32_t T,
  *   levels_out int32 / budgets_out double: HOST [n_seqs*T] or NULL
  *         (budgets are NaN in fixed mode)
  *   conf_trace float / argmax_trace int32: device [T, n_seqs*L] or NULL.
- * Errors: as the calls it makes; EINVAL for a bad schedule argument. */
+ *   mailbox: from davet_mailbox_create; required in policy mode with T > 1,
+ *            ignored (may be NULL) otherwise.
+ * Errors: as the calls it makes; EINVAL for a bad schedule argument or a
+ * missing mailbox; EHIP when a wait for published levels fails or exceeds
+ * the wait limit. */
 int davet_run_schedule(const davet_model_cfg* cfg, const davet_weights* w,
                        int32_t n_seqs, const davet_view_geom* geoms,
                        const void* const* visual, void* const* view_bufs,
@@ -426,7 +460,8 @@ int davet_run_schedule(const davet_model_cfg* cfg, const davet_weights* w,
                        int32_t* resp_ids, uint8_t* resp_masked,
                        int32_t* levels_out, double* budgets_out,
                        float* conf_trace, int32_t* argmax_trace,
-                       void* workspace, size_t ws_bytes, hipStream_t stream);
+                       davet_mailbox* mailbox, void* workspace,
+                       size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------ profiling -- */
 

@@ -8,7 +8,8 @@ from ._lib import (  # noqa: F401
     DAVET_BF16, DAVET_F16, DAVET_F32, DAVET_HEAD_ROWS, DAVET_HEAD_TILED,
     DAVET_REALIZER_MERGE, DAVET_REALIZER_POOL, DAVET_REALIZER_PRUNE,
     MAX_REALIZER_GRID, MAX_SEQS, EXPORTED, LIB_PATH, DavetError,
-    LayerWeights, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
+    LayerWeights, Mailbox, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
+    davet_set_wait_limit, default_mailbox,
     davet_build_views, davet_convert, davet_demand_prior, davet_denoise_step,
     davet_head_tiled_elems, davet_pack_head, davet_parse_operation,
     davet_policy_envelope, davet_policy_step, davet_policy_step_device,

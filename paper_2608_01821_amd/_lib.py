@@ -121,8 +121,11 @@ _SIGS = {
                                      _i32, C.POINTER(ViewGeom), _P_vp, _P_vp,
                                      _vp, _P_i32, _i32, _i32, _i32,
                                      C.POINTER(Policy), _P_i32, _vp, _vp,
-                                     _P_i32, _P_f64, _vp, _vp, _vp,
+                                     _P_i32, _P_f64, _vp, _vp, _vp, _vp,
                                      C.c_size_t, _vp]),
+    "davet_mailbox_create": (C.c_int, [_P_vp]),
+    "davet_mailbox_destroy": (C.c_int, [_vp]),
+    "davet_set_wait_limit": (C.c_int, [C.c_double]),
     "davet_prof_enable": (C.c_int, [_i32]),
     "davet_prof_reset": (C.c_int, []),
     "davet_prof_only": (C.c_int, [_i32]),
@@ -377,11 +380,50 @@ def davet_policy_step_device(pols, t, T, lower, upper, conf, argmax,
         _stream(stream)))
 
 
+class Mailbox:
+    """A davet_mailbox (pinned host memory the policy-mode loop writes the
+    next levels into), made once and freed by close() or at exit."""
+
+    def __init__(self):
+        h = C.c_void_p()
+        _check(_L.davet_mailbox_create(C.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle is not None and self.handle.value:
+            h, self.handle = self.handle, None
+            _check(_L.davet_mailbox_destroy(h))
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+_MAILBOX = None
+
+
+def default_mailbox():
+    """The process's mailbox, made on first use (a set-up step, not part of
+    a loop's steady state)."""
+    global _MAILBOX
+    if _MAILBOX is None:
+        _MAILBOX = Mailbox()
+    return _MAILBOX
+
+
+def davet_set_wait_limit(seconds):
+    _check(_L.davet_set_wait_limit(float(seconds)))
+
+
 def davet_run_schedule(cfg, weights: Weights, geoms, visual, view_bufs,
                        prompt_ids, cu_prompt, L, T, k, pols, fixed_levels,
                        resp_ids, resp_masked, workspace, conf_trace=None,
-                       argmax_trace=None, stream=None):
-    """Returns (levels [n_seqs*T], budgets [n_seqs*T]) as host lists."""
+                       argmax_trace=None, stream=None, mailbox=None):
+    """Returns (levels [n_seqs*T], budgets [n_seqs*T]) as host lists.
+    ``mailbox``: a Mailbox; in policy mode the process's default one when
+    None."""
     n = len(visual)
     g = (ViewGeom * n)(*geoms)
     p = (Policy * n)(*pols) if pols is not None else None
@@ -389,11 +431,14 @@ def davet_run_schedule(cfg, weights: Weights, geoms, visual, view_bufs,
         if fixed_levels is not None else None
     lv = (C.c_int32 * (n * T))()
     bu = (C.c_double * (n * T))()
+    if mailbox is None and pols is not None:
+        mailbox = default_mailbox()
+    mb = None if mailbox is None else mailbox.handle
     _check(_L.davet_run_schedule(
         C.byref(cfg), C.byref(weights.struct), n, g, _ptr_array(visual),
         _ptr_array(view_bufs), _ptr(prompt_ids), _i32_array(cu_prompt),
         int(L), int(T), int(k), p, fl, _ptr(resp_ids), _ptr(resp_masked),
-        lv, bu, _ptr(conf_trace), _ptr(argmax_trace), _ptr(workspace),
+        lv, bu, _ptr(conf_trace), _ptr(argmax_trace), mb, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
     return list(lv), list(bu)
 

@@ -3,20 +3,35 @@
 // schedule, or the allocation policy from the previous step's signals), runs
 // the denoiser and commits.  In policy mode the GPU forms the risk signals
 // and the next allocation after each commitment (launch_policy_step) and
-// writes the next levels and budgets into pinned host memory, then a stamp;
-// the host polls the stamp (the only crossing per step: the next step's
-// launch sizes depend on the levels) and enqueues the next step.
+// writes the next levels and budgets into the caller's mailbox (pinned,
+// host-coherent memory from davet_mailbox_create), then a stamp; the host
+// polls the stamp (the only crossing per step: the next step's launch sizes
+// depend on the levels) and enqueues the next step.  The loop itself
+// allocates and frees nothing.
 
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstddef>
 #include <string>
 #include <vector>
 
 #include "common.h"
+
+// What the device policy step publishes for the host (one per mailbox).
+struct davet_mailbox {
+  struct Data {
+    int32_t level[DAVET_MAX_SEQS];
+    double budget[DAVET_MAX_SEQS];
+    int32_t done;                    // stamp of the last step published
+  };
+  Data* host = nullptr;              // pinned, host-coherent
+  Data* dev = nullptr;               // its device address
+  uint32_t next_stamp = 1;           // stamps are unique per mailbox
+};
 
 namespace davet {
 void schedule_scratch(const davet_model_cfg* c, int64_t tokens, int64_t seqs,
@@ -38,12 +53,20 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       size_t ws_bytes, const float* rope_cs, int rows_bound,
                       hipStream_t stream);
 
+// Host-side limit on one wait for a step's published levels (seconds).
+static std::atomic<double> g_wait_limit_s{120.0};
+
 // Waits until the GPU has published `want` to the pinned word *flag.  Polls
 // the word (its writer fences at system scope first, so the data it guards
-// is complete) and, every few thousand polls, the stream: an error on the
-// stream, or a stream that drained without the stamp, ends the wait.
+// is complete) and, every few thousand polls, the stream and the clock: an
+// error on the stream, a stream that drained without the stamp, or a wait
+// longer than the limit ends it with DAVET_EHIP.  After a time-out the
+// step's kernels may still be running and will still write the mailbox.
 static int wait_stamp(const volatile int32_t* flag, int32_t want,
                       hipStream_t s) {
+  using clock = std::chrono::steady_clock;
+  const auto t0 = clock::now();
+  const double limit = g_wait_limit_s.load(std::memory_order_relaxed);
   for (unsigned spin = 1;; ++spin) {
     if (*flag == want) break;
     __builtin_ia32_pause();
@@ -55,11 +78,62 @@ static int wait_stamp(const volatile int32_t* flag, int32_t want,
       if (q == hipSuccess && *flag != want)
         return set_error(DAVET_EHIP, "davet_run_schedule: the policy step "
                                      "ended without publishing its levels");
+      const double waited =
+          std::chrono::duration<double>(clock::now() - t0).count();
+      if (waited > limit && *flag != want)
+        return set_error(
+            DAVET_EHIP,
+            "davet_run_schedule: no levels published within " +
+                std::to_string(limit) +
+                " s (the stream is still running; synchronise it before "
+                "reusing or destroying the mailbox)");
     }
   }
   std::atomic_thread_fence(std::memory_order_acquire);
   return DAVET_OK;
 }
+}  // namespace davet
+
+extern "C" int davet_mailbox_create(davet_mailbox** out) {
+  using namespace davet;
+  DAVET_CHECK_ARG(out, DAVET_EINVAL, "davet_mailbox_create: out is null");
+  *out = nullptr;
+  davet_mailbox* mb = new (std::nothrow) davet_mailbox();
+  DAVET_CHECK_ARG(mb, DAVET_ENOMEM, "davet_mailbox_create: out of host memory");
+  hipError_t e = hipHostMalloc((void**)&mb->host, sizeof(davet_mailbox::Data),
+                               hipHostMallocCoherent);
+  if (e == hipSuccess)
+    e = hipHostGetDevicePointer((void**)&mb->dev, mb->host, 0);
+  if (e != hipSuccess) {
+    if (mb->host) (void)hipHostFree(mb->host);
+    delete mb;
+    return set_error(DAVET_EHIP, std::string("davet_mailbox_create: ") +
+                                     hipGetErrorString(e));
+  }
+  mb->host->done = 0;
+  *out = mb;
+  return DAVET_OK;
+}
+
+extern "C" int davet_mailbox_destroy(davet_mailbox* mb) {
+  using namespace davet;
+  if (!mb) return DAVET_OK;
+  // a policy step still queued on some stream may write the mailbox
+  const hipError_t e1 = hipDeviceSynchronize();
+  const hipError_t e2 = hipHostFree(mb->host);
+  delete mb;
+  if (e1 != hipSuccess || e2 != hipSuccess)
+    return set_error(DAVET_EHIP, std::string("davet_mailbox_destroy: ") +
+                                     hipGetErrorString(e1 != hipSuccess ? e1 : e2));
+  return DAVET_OK;
+}
+
+extern "C" int davet_set_wait_limit(double seconds) {
+  using namespace davet;
+  DAVET_CHECK_ARG(seconds > 0.0 && std::isfinite(seconds), DAVET_EINVAL,
+                  "davet_set_wait_limit: seconds must be positive and finite");
+  g_wait_limit_s.store(seconds, std::memory_order_relaxed);
+  return DAVET_OK;
 }
 
 extern "C" int davet_run_schedule(
@@ -69,8 +143,8 @@ extern "C" int davet_run_schedule(
     int32_t L, int32_t T, int32_t k, const davet_policy* pols,
     const int32_t* fixed_levels, int32_t* resp_ids, uint8_t* resp_masked,
     int32_t* levels_out, double* budgets_out, float* conf_trace,
-    int32_t* argmax_trace, void* workspace, size_t ws_bytes,
-    hipStream_t stream) {
+    int32_t* argmax_trace, davet_mailbox* mailbox, void* workspace,
+    size_t ws_bytes, hipStream_t stream) {
   using namespace davet;
   DAVET_CHECK_ARG(cfg && w && geoms && visual && cu_prompt && resp_ids &&
                       resp_masked && workspace,
@@ -83,6 +157,9 @@ extern "C" int davet_run_schedule(
                   "davet_run_schedule: give exactly one of pols, fixed_levels");
   DAVET_CHECK_ARG(L >= 1 && L <= DAVET_MAX_RESP, DAVET_ESHAPE,
                   "davet_run_schedule: L out of range");
+  DAVET_CHECK_ARG(!pols || T == 1 || mailbox, DAVET_EINVAL,
+                  "davet_run_schedule: policy mode needs a mailbox "
+                  "(davet_mailbox_create)");
   const int K = geoms[0].K;
   DAVET_CHECK_ARG(K >= 1 && K <= DAVET_MAX_LEVELS, DAVET_ESHAPE,
                   "davet_run_schedule: K out of range");
@@ -144,18 +221,9 @@ extern "C" int davet_run_schedule(
   }
 
   // policy state: envelopes on the host (once per sample), the per-step
-  // signals and allocation on the GPU, the next levels in pinned memory
-  struct Mailbox {
-    int32_t level[DAVET_MAX_SEQS];
-    double budget[DAVET_MAX_SEQS];
-    int32_t done;                    // the last step whose levels are in
-  };
-  struct PinnedMailbox {
-    Mailbox* p = nullptr;
-    ~PinnedMailbox() { if (p) (void)hipHostFree(p); }
-  } mail;
-  Mailbox* mail_dev = nullptr;
+  // signals and allocation on the GPU, the next levels in the mailbox
   std::vector<double> lower, upper, alpha(n_seqs), lo_t(n_seqs), up_t(n_seqs);
+  uint32_t stamp0 = 0;
   if (pols) {
     lower.resize((size_t)n_seqs * T);
     upper.resize((size_t)n_seqs * T);
@@ -168,10 +236,11 @@ extern "C" int davet_run_schedule(
       alpha[s] = pols[s].alpha;
     }
     if (T > 1) {
-      DAVET_HIP(hipHostMalloc((void**)&mail.p, sizeof(Mailbox),
-                              hipHostMallocCoherent));
-      DAVET_HIP(hipHostGetDevicePointer((void**)&mail_dev, mail.p, 0));
-      mail.p->done = 0;
+      // this call's stamps: stamp0 + t for t = 1..T-1, never reused by the
+      // mailbox, so a late write of an earlier (failed) call cannot pass
+      stamp0 = mailbox->next_stamp;
+      mailbox->next_stamp += (uint32_t)T;
+      if (mailbox->next_stamp > 0x7fff0000u) mailbox->next_stamp = 1;
     }
   }
   int32_t* am_buf[2] = {reinterpret_cast<int32_t*>(ws + am_off),
@@ -190,8 +259,8 @@ extern "C" int davet_run_schedule(
                                    nullptr);
         if (rc) return rc;
       } else if (pols) {
-        lv = mail.p->level[s];
-        b = mail.p->budget[s];
+        lv = mailbox->host->level[s];
+        b = mailbox->host->budget[s];
         DAVET_CHECK_ARG(lv >= 0 && lv < K, DAVET_EHIP,
                         "davet_run_schedule: device policy returned a level "
                         "out of range");
@@ -229,16 +298,14 @@ extern "C" int davet_run_schedule(
         lo_t[s] = lower[(size_t)s * T + t];
         up_t[s] = upper[(size_t)s * T + t];
       }
-      char* md = reinterpret_cast<char*>(mail_dev);
-      rc = launch_policy_step(
-          n_seqs, L, K, alpha.data(), lo_t.data(), up_t.data(), conf, am,
-          am_prev, resp_masked,
-          reinterpret_cast<int32_t*>(md + offsetof(Mailbox, level)),
-          reinterpret_cast<double*>(md + offsetof(Mailbox, budget)), nullptr,
-          nullptr, nullptr,
-          reinterpret_cast<int32_t*>(md + offsetof(Mailbox, done)), t, stream);
+      davet_mailbox::Data* md = mailbox->dev;
+      const int32_t stamp = (int32_t)(stamp0 + (uint32_t)t);
+      rc = launch_policy_step(n_seqs, L, K, alpha.data(), lo_t.data(),
+                              up_t.data(), conf, am, am_prev, resp_masked,
+                              md->level, md->budget, nullptr, nullptr, nullptr,
+                              &md->done, stamp, stream);
       if (rc) return rc;
-      rc = wait_stamp(&mail.p->done, t, stream);
+      rc = wait_stamp(&mailbox->host->done, stamp, stream);
       if (rc) return rc;
     }
   }

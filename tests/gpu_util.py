@@ -4,8 +4,11 @@ compute mode, the oracle-side values, and the comparison rules.
 Compute modes: "f32" (the fp32 configuration), "f16" and "bf16" (16-bit
 matrix-core operands).  A bf16 model runs in either 16-bit mode; in "f16"
 mode its bf16 weights and encodings are converted to fp16 (round to nearest
-even, exact for every value with |x| >= 2^-17) and the oracle is fed the
-very same converted values.
+even, exact for every value with |x| >= 2^-17).  The oracle is fed either
+the very same converted values (``oracle_values="device"``, the default of
+the small-shape tests) or the model's own bf16-rounded values
+(``oracle_values="model"``: the conversion, and the fp16 rounding of the
+pooled views, then sit inside the measured error).
 
 Comparison rules (floating point decides an integer, so the argmax is
 compared where it is unique at the tolerance, and checked for validity
@@ -68,16 +71,26 @@ def view_geom(cfg, n_crops, mode=None, mixed_stride=0, realizer=0):
 
 class Model:
     """Seeded weights on both sides in one compute mode.  ``host`` feeds the
-    oracle the exact values the device holds -- in memory, or regenerated per
-    layer on demand when ``stream_host`` is set (large stacks)."""
+    oracle the values the device holds (oracle_values="device") or the
+    model's own values as generated (oracle_values="model": bf16-rounded for
+    a bf16 model) -- in memory, or regenerated per layer on demand when
+    ``stream_host`` is set (large stacks)."""
 
-    def __init__(self, cfg, mode=None, keep_host=True, stream_host=False):
+    def __init__(self, cfg, mode=None, keep_host=True, stream_host=False,
+                 oracle_values="device"):
+        assert oracle_values in ("device", "model")
         self.cfg = cfg
         self.mode = mode = mode or default_mode(cfg)
+        self.oracle_values = oracle_values
+
+        def host_of(a):
+            if oracle_values == "model":
+                return np.ascontiguousarray(a, np.float32)
+            return to_mode(a, mode)[1]
 
         def both(a):
-            dev, host = to_mode(a, mode)
-            return torch.from_numpy(dev).cuda(), host
+            dev, _ = to_mode(a, mode)
+            return torch.from_numpy(dev).cuda(), host_of(a)
 
         self.dev_layers = []
         host_layers = []
@@ -96,7 +109,7 @@ class Model:
         if keep_host:
             if stream_host:
                 def layers(i):
-                    return {k: to_mode(v, mode)[1] for k, v in
+                    return {k: host_of(v) for k, v in
                             synth.gen_layer_weights(cfg, i).items()}
             else:
                 layers = host_layers
@@ -104,22 +117,32 @@ class Model:
 
 
 class Sample:
-    """One sample's inputs on both sides and its GPU-built views."""
+    """One sample's inputs on both sides and its GPU-built views.  With
+    oracle_values="model" the oracle's views are built from the encoding as
+    generated (bf16-rounded for a bf16 model) and kept at float32 (the
+    float64 window means rounded once to fp32, 2^-24 relative): the
+    oracle's inputs are the model's own, and whatever precision the GPU
+    stores its views in sits inside the measured error."""
 
     def __init__(self, cfg, n_crops, visual, prompt, mode=None,
-                 mixed_stride=0, realizer=0):
+                 mixed_stride=0, realizer=0, oracle_values="device"):
         self.cfg = cfg
         self.mode = mode = mode or default_mode(cfg)
         dev_v, host_v = to_mode(visual, mode)
+        ref_dtype = mode
+        if oracle_values == "model":
+            host_v = np.ascontiguousarray(visual, np.float32)
+            ref_dtype = "f32"
         self.visual = host_v
         self.prompt = prompt
         self.n_crops = n_crops
         if realizer:
             self.ref_levels, _ = realizers.build_views(
-                host_v, n_crops, cfg.grid, cfg.K, realizer, mode)
+                host_v, n_crops, cfg.grid, cfg.K, realizer, ref_dtype)
         else:
             self.ref_levels, _ = views.build_views(host_v, n_crops, cfg.grid,
-                                                   cfg.K, mode, mixed_stride)
+                                                   cfg.K, ref_dtype,
+                                                   mixed_stride)
         geom = view_geom(cfg, n_crops, mode, mixed_stride, realizer)
         self.sizes = dv.davet_view_sizes(geom)
         self.dev_v = torch.from_numpy(dev_v).cuda()

@@ -3,8 +3,10 @@ bench times (same packed batch, same kernels), on sampled outputs the oracle
 computes one by one: the oracle runs the whole layer stack for the sampled
 sequence (attention needs every position) but projects only sampled masked
 rows on the vocabulary.  Teacher-forced; the bf16 model runs in the fp16
-operand mode (its weights converted exactly) and must reach logits rel-RMS
-<= 1e-2 against the oracle fed the same values.
+operand mode (its bf16 weights rounded to fp16, exact for |w| >= 2^-17) and
+must reach logits rel-RMS <= 1e-2 against the oracle fed the model's own
+bf16-rounded weights and encodings (so the conversion and the fp16 views sit
+inside the measured error).
 """
 
 import sys
@@ -82,9 +84,10 @@ def check_sampled(cfg, mdl, sample, level, ids, masked, g_conf, g_am,
 def one_layer(request):
     cfg = synth.get_config(request.param)
     say("generating config %d" % cfg.cid)
-    mdl = Model(cfg)
+    mdl = Model(cfg, oracle_values="model")
     s = synth.gen_sample(cfg)
-    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0])
+    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0],
+                    oracle_values="model")
     return cfg, mdl, sample
 
 
@@ -110,9 +113,9 @@ def test_ragged16_full_size():
     and the same confidences up to the regrouping of the softmax sum."""
     cfg = synth.get_config(5)
     say("generating config 5")
-    mdl = Model(cfg)
+    mdl = Model(cfg, oracle_values="model")
     s = synth.gen_sample(cfg)
-    samples = [Sample(cfg, c, v, p) for c, v, p in
+    samples = [Sample(cfg, c, v, p, oracle_values="model") for c, v, p in
                zip(s["n_crops"], s["visual"], s["prompts"])]
     rng = np.random.default_rng(55)
     levels = [int(x) for x in rng.integers(0, cfg.K, len(samples))]
@@ -140,27 +143,48 @@ def test_ragged16_full_size():
     assert bool(torch.equal(t_lg, g_lg))
 
 
-def test_stack32_full_size_low_view():
-    """The 32-layer 8B-shaped stack at the coarse view: bf16 error growth
-    over the whole depth stays inside the tolerance."""
+@pytest.fixture(scope="module")
+def stack32():
+    """The 32-layer 8B-shaped stack on the device (fp16 operands, ~16 GB),
+    built once for the three view levels; the oracle regenerates each
+    layer's bf16 weights as it reaches it."""
     cfg = synth.get_config(4)
     say("generating config 4 (32 layers)")
-    mdl = Model(cfg, stream_host=True)
+    mdl = Model(cfg, stream_host=True, oracle_values="model")
     gen = mdl.host["layers"]
 
     def layer_with_progress(i):
-        if i % 8 == 0:
+        if i % 4 == 0:
             say("  oracle layer %d / %d" % (i, cfg.n_layers))
         return gen(i)
     mdl.host["layers"] = layer_with_progress
     s = synth.gen_sample(cfg)
-    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0])
-    ids = np.full(cfg.resp_len, cfg.mask_id, np.int32)
-    masked = np.ones(cfg.resp_len, np.uint8)
-    g_conf, g_am, g_lg = gpu_step(cfg, mdl, [sample], [0], ids[None],
+    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0],
+                    oracle_values="model")
+    return cfg, mdl, sample
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("level", [0, 1, 2])
+def test_stack32_full_size(stack32, level):
+    """The 32-layer 8B-shaped stack at each view level (372, 960 and 3092
+    tokens): the first step of the loop (all positions masked) at the coarse
+    view, a partly committed answer at the middle and full views.  The error
+    of 32 layers of 16-bit operands stays inside the tolerance at the
+    longest sequence, where the projections run their 256 x 256 tiles
+    without a K split."""
+    cfg, mdl, sample = stack32
+    rng = np.random.default_rng(40 + level)
+    if level == 0:
+        ids = np.full(cfg.resp_len, cfg.mask_id, np.int32)
+        masked = np.ones(cfg.resp_len, np.uint8)
+    else:
+        ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab,
+                                   0.5 if level == 1 else 0.9)
+    g_conf, g_am, g_lg = gpu_step(cfg, mdl, [sample], [level], ids[None],
                                   masked[None])
-    check_sampled(cfg, mdl, sample, 0, ids, masked, g_conf[0], g_am[0],
-                  g_lg[0], 8, 4)
+    check_sampled(cfg, mdl, sample, level, ids, masked, g_conf[0], g_am[0],
+                  g_lg[0], 8, 4 + level)
 
 
 def test_tiled_head_full_size_bit_identical(one_layer):

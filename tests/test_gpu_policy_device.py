@@ -1,8 +1,10 @@
 """The closed-loop policy step on the GPU (Sec. 4.2: signals c̄ and χ after a
-commitment, then Eqs. 7-9 for the next step) against the host functions
-davet_step_stats + davet_policy_step, bit for bit, on seeded inputs chosen
-so that any change of summation order or any fused multiply-add would show:
-confidences spanning many binades, empty masked sets, unchanged and changed
+commitment, then Eqs. 7-9 for the next step) against the oracle
+(oracle.policy.envelope, oracle.stats.mean_conf / churn, oracle.policy.step)
+and against the library's host functions davet_step_stats +
+davet_policy_step, bit for bit, on seeded inputs chosen so that any change
+of summation order or any fused multiply-add would show: confidences
+spanning many binades, empty masked sets, unchanged and changed
 predictions, budgets near the Eq. 9 thresholds, and K = 1..4."""
 
 import numpy as np
@@ -10,6 +12,8 @@ import pytest
 import torch
 
 import paper_2608_01821_amd as dv
+from oracle import policy as opol
+from oracle import stats as ostats
 
 pytestmark = pytest.mark.gpu
 
@@ -41,7 +45,8 @@ def test_device_policy_step_matches_host(n, L, K, T, seed):
     lower = np.empty(n * T)
     upper = np.empty(n * T)
     for s, p in enumerate(pols):
-        lo, up = dv.davet_policy_envelope(p, T)
+        lo, up = opol.envelope(T, bool(p.early), p.B, p.rho, p.demand)
+        assert (lo, up) == tuple(dv.davet_policy_envelope(p, T))
         lower[s * T:(s + 1) * T] = lo
         upper[s * T:(s + 1) * T] = up
     for t in sorted({1, min(2, T - 1), T - 1}):
@@ -68,14 +73,23 @@ def test_device_policy_step_matches_host(n, L, K, T, seed):
         g_lv, g_bu, g_r = lv.cpu().numpy(), bu.cpu().numpy(), rr.cpu().numpy()
         for s in range(n):
             o = slice(s * L, (s + 1) * L)
+            lo_s = lower[s * T:(s + 1) * T].tolist()
+            up_s = upper[s * T:(s + 1) * T].tolist()
+            # the oracle's signals and next-step allocation
+            ocb = ostats.mean_conf(conf[o], masked[o])
+            och = ostats.churn(am[o], prev[o], masked[o], t == 1)
+            ob, olv, orr = opol.step(t + 1, lo_s, up_s, pols[s].alpha, ocb,
+                                     och, K)
+            assert g_bu[s] == ob and g_r[s] == orr, (t, s, g_bu[s], ob)
+            assert g_lv[s] == olv
+            # and the library's host policy, on the same signals
             cb, ch = dv.davet_step_stats(conf[o], am[o],
                                          None if t == 1 else prev[o],
                                          masked[o])
-            b, l_, r = dv.davet_policy_step(pols[s], t + 1, T,
-                                            lower[s * T:(s + 1) * T],
-                                            upper[s * T:(s + 1) * T], cb, ch)
-            assert g_bu[s] == b and g_r[s] == r, (t, s, g_bu[s], b)
-            assert g_lv[s] == l_
+            assert (cb, ch) == (ocb, och)
+            b, l_, r = dv.davet_policy_step(pols[s], t + 1, T, lo_s, up_s,
+                                            cb, ch)
+            assert (b, l_, r) == (ob, olv, orr)
 
 
 def test_device_policy_step_argument_checks():

@@ -6,9 +6,10 @@
    confidences (rounded to float32, the kernel's precision) and must select
    exactly what the oracle selects from the same float32 values.
 2. Free-running ``davet_run_schedule`` (fixed schedule and policy mode):
-   schedule, per-step reveal counts and flag monotonicity hold exactly; the
-   policy's levels/budgets equal what the library's host policy gives for the
-   run's own confidence trace; step 1 (identical inputs on both sides)
+   schedule, per-step reveal counts and flag monotonicity hold exactly; at
+   every step the policy's levels/budgets equal what the oracle's policy
+   (oracle.stats + oracle.policy) gives for the run's own confidence trace;
+   step 1 (identical inputs on both sides)
    matches the oracle; and later steps match it for as long as the two
    trajectories coincide.
 """
@@ -23,6 +24,8 @@ from gpu_util import (TOL, Model, Sample, compare, dev_tensor, model_cfg,
                       oracle_step, run_gpu_step, to_mode, view_geom,
                       workspace)
 from oracle import decode, loop
+from oracle import policy as opol
+from oracle import stats as ostats
 
 pytestmark = pytest.mark.gpu
 
@@ -158,6 +161,23 @@ def _trajectory_prefix_match(cfg, ref_tr, conf_tr, am_tr, final_masked, s):
     return n_ok
 
 
+def _check_policy_trace(cfg, pols, lv, bu, ctr, atr, msk):
+    """Every step's level and budget of every sequence equal the oracle's
+    allocation (oracle.policy) from the signals (oracle.stats) of the run's
+    own previous step: its confidence and prediction traces."""
+    T = cfg.steps
+    for i, pol in enumerate(pols):
+        lo, up = opol.envelope(T, bool(pol.early), pol.B, pol.rho, pol.demand)
+        cb, ch = 0.0, 0.0
+        for t in range(1, T + 1):
+            b, l_, _ = opol.step(t, lo, up, pol.alpha, cb, ch, cfg.K)
+            assert b == bu[i, t - 1] and l_ == lv[i, t - 1], (i, t)
+            after = np.isfinite(ctr[t, i]) if t < T else msk[i].astype(bool)
+            cb = ostats.mean_conf(ctr[t - 1, i], after)
+            ch = ostats.churn(atr[t - 1, i], None if t == 1 else
+                              atr[t - 2, i], after, t == 1)
+
+
 def test_run_schedule_fixed_tiny():
     cfg = synth.get_config(1)
     mdl = Model(cfg)
@@ -185,16 +205,8 @@ def test_run_schedule_policy_ragged(cid):
     lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
     _check_invariants(cfg, ctr, atr, ids, msk)
     T, L = cfg.steps, cfg.resp_len
+    _check_policy_trace(cfg, pols, lv, bu, ctr, atr, msk)
     for i, pol in enumerate(pols):
-        lo, up = dv.davet_policy_envelope(pol, T)
-        cb, ch = 0.0, 0.0
-        for t in range(1, T + 1):
-            b, l_, _ = dv.davet_policy_step(pol, t, T, lo, up, cb, ch)
-            assert b == bu[i, t - 1] and l_ == lv[i, t - 1]
-            after = np.isfinite(ctr[t, i]) if t < T else msk[i].astype(bool)
-            cb, ch = dv.davet_step_stats(ctr[t - 1, i], atr[t - 1, i],
-                                         None if t == 1 else atr[t - 2, i],
-                                         after.astype(np.uint8))
         ref = loop.run_sequence(cfg, mdl.host,
                                 to_mode(s["visual"][i], mdl.mode)[1],
                                 s["n_crops"][i], s["prompts"][i], T, cfg.k,
@@ -220,6 +232,7 @@ def test_run_schedule_head_over_several_row_tiles():
                       1 if p["early"] else 0, cfg.K) for c in s["categories"]]
     lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
     _check_invariants(cfg, ctr, atr, ids, msk)
+    _check_policy_trace(cfg, pols, lv, bu, ctr, atr, msk)
     assert cfg.n_seqs * cfg.resp_len > 3 * 128
     for i, pol in enumerate(pols):
         ref = loop.run_sequence(cfg, mdl.host,
@@ -258,6 +271,7 @@ def test_run_schedule_tiled_head():
     lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols,
                                                weights=w_tiled)
     _check_invariants(cfg, ctr, atr, ids, msk)
+    _check_policy_trace(cfg, pols, lv, bu, ctr, atr, msk)
     assert np.array_equal(lv[:, 0], lv_r[:, 0])
     assert np.array_equal(atr[0], atr_r[0])
     assert_conf_regrouped(ctr[0], ctr_r[0])
@@ -287,6 +301,7 @@ def test_run_schedule_64_sequences():
                       1 if p["early"] else 0, cfg.K) for c in s["categories"]]
     lv, bu, ctr, atr, ids, msk = _run_schedule(cfg, mdl, s, pols=pols)
     _check_invariants(cfg, ctr, atr, ids, msk)
+    _check_policy_trace(cfg, pols, lv, bu, ctr, atr, msk)
     for i in (0, 31, 63):
         ref = loop.run_sequence(cfg, mdl.host,
                                 to_mode(s["visual"][i], mdl.mode)[1],

@@ -83,6 +83,29 @@ def test_step_stats_bit_exact_vs_oracle(data, L, first):
     assert ch == ostats.churn(am, prev, m, first)
 
 
+@settings(max_examples=150, deadline=None)
+@given(data=st.data(), L=st.integers(0, 1024), first=st.booleans(),
+       power=st.sampled_from([1, 8, 24]))
+def test_step_stats_bit_exact_vs_oracle_long(data, L, first, power):
+    """Up to the library's largest response (1024 positions), with
+    confidences spread over many binades (u^8, u^24) so that the float64
+    sum's rounding depends on the order of its terms; exact zeros, ones and
+    the smallest subnormal mixed in."""
+    rng = np.random.default_rng(data.draw(st.integers(0, 2 ** 31)))
+    conf = (rng.random(L) ** power).astype(np.float32)
+    if L:
+        special = np.array([0.0, 1.0, np.float32(1e-45), 0.5], np.float32)
+        idx = rng.integers(0, L, min(L, 8))
+        conf[idx] = special[rng.integers(0, 4, len(idx))]
+    am = rng.integers(0, 126464, L).astype(np.int32)
+    prev = np.where(rng.random(L) < 0.8, am,
+                    rng.integers(0, 126464, L)).astype(np.int32)
+    m = (rng.random(L) < data.draw(st.floats(0.0, 1.0))).astype(np.uint8)
+    cb, ch = dv.davet_step_stats(conf, am, None if first else prev, m)
+    assert cb == ostats.mean_conf(conf, m)
+    assert ch == ostats.churn(am, prev, m, first)
+
+
 def _expect(status, fn, *a, **k):
     with pytest.raises(dv.DavetError) as e:
         fn(*a, **k)
@@ -127,6 +150,38 @@ def test_argument_validation_without_gpu():
     _expect(-1, dv.davet_policy_step, pol, 5, 4, lo, up, 0.0, 0.0)
     _expect(-1, dv.davet_policy_step, _pol(0.75, 0.2, 1, 1, True, 9), 1, 4,
             lo, up, 0.0, 0.0)
+
+
+def test_schedule_mailbox_and_wait_limit_checks():
+    """Policy mode needs a caller-owned mailbox (the loop allocates nothing);
+    the wait limit must be positive and finite.  No HIP call is made."""
+    import ctypes as C
+    lib = dv.raw()
+    _expect(-1, dv.davet_set_wait_limit, 0.0)
+    _expect(-1, dv.davet_set_wait_limit, -1.0)
+    _expect(-1, dv.davet_set_wait_limit, math.inf)
+    _expect(-1, dv.davet_set_wait_limit, math.nan)
+    dv.davet_set_wait_limit(120.0)
+    assert lib.davet_mailbox_create(None) == -1
+    assert lib.davet_mailbox_destroy(None) == 0
+    cfg = dv.ModelCfg(1, 256, 2, 128, 512, 1000, 999, 1e-5, 1e4,
+                      dv.DAVET_F16)
+    w = dv.WeightsT(16, 16, None, None, 0)
+    g = (dv.ViewGeom * 1)(dv.ViewGeom(1, 7, 256, 3, dv.DAVET_F16))
+    ptrs = (C.c_void_p * 2)(256, 256)
+    cu = (C.c_int32 * 2)(0, 4)
+    pol = (dv.Policy * 1)(_pol(0.75, 0.2, 1.0, 1.0, True))
+    fixed = (C.c_int32 * 4)(0, 1, 2, 0)
+
+    def call(pols, fixed_levels, T, mailbox):
+        return lib.davet_run_schedule(
+            C.byref(cfg), C.byref(w), 1, g, ptrs, ptrs, C.c_void_p(256), cu,
+            8, T, 2, pols, fixed_levels, C.c_void_p(256), C.c_void_p(256),
+            None, None, None, None, mailbox, C.c_void_p(256), 1 << 20, None)
+    assert call(pol, None, 4, None) == -1
+    assert "mailbox" in dv.raw().davet_last_error().decode()
+    assert call(pol, fixed, 4, None) == -1      # both schedules given
+    assert call(None, None, 4, None) == -1      # neither
 
 
 def test_head_tiling_host_checks():
