@@ -241,6 +241,26 @@ int davet_realizer_key_count(const davet_view_geom* g, int32_t* n_keys);
 int davet_realizer_keys(const davet_view_geom* g, const void* v,
                         double* keys, hipStream_t stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): davet_build_views with
+ * the prune / merge realizers' scratch (davet_views_scratch_bytes: keys and
+ * the maps of the pooled levels) in a device array the library holds, of
+ * DAVET_STATIC_SCRATCH_BYTES per GPU, kept until the process ends.  Same
+ * arguments and results as davet_build_views without scratch; the call
+ * allocates nothing.  The first call on a device resolves the array's
+ * address there (a one-time set-up step that may load the library's code
+ * object: make it before capturing).  All calls on one device share its
+ * array: calls that overlap on one device (other streams, other threads)
+ * race; consecutive calls on one stream are safe (everything a call reads
+ * from the array it first writes).  Pooling needs no scratch and never
+ * touches the array.  Errors: as davet_build_views, and ENOMEM when the
+ * geometry needs more scratch than the maximum (e.g. the merge realizer on
+ * more than ~40 crops of a 64 x 64 grid). */
+#define DAVET_STATIC_SCRATCH_BYTES (4u << 20)
+int davet_build_views_static(const davet_view_geom* g, const void* v,
+                             void* const* levels, int32_t* const* idx_offsets,
+                             int32_t* const* idx_members, hipStream_t stream);
+
 /* Index maps of all K levels from given keys (device float64 [n_keys]),
  * deterministic for identical keys.  Keys are ordered larger first, equal
  * keys by lower index, NaN as -inf, -0 as +0.  Per crop and level l with

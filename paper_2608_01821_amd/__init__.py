@@ -7,10 +7,10 @@ arguments (see ``_lib``).  Import fails loudly if the library is not built.
 from ._lib import (  # noqa: F401
     DAVET_BF16, DAVET_F16, DAVET_F32, DAVET_HEAD_ROWS, DAVET_HEAD_TILED,
     DAVET_REALIZER_MERGE, DAVET_REALIZER_POOL, DAVET_REALIZER_PRUNE,
-    MAX_REALIZER_GRID, MAX_SEQS, EXPORTED, LIB_PATH, DavetError,
+    MAX_REALIZER_GRID, MAX_SEQS, STATIC_SCRATCH_BYTES, EXPORTED, LIB_PATH, DavetError,
     LayerWeights, Mailbox, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
     davet_set_wait_limit, default_mailbox,
-    davet_build_views, davet_convert, davet_demand_prior, davet_denoise_step,
+    davet_build_views, davet_build_views_static, davet_convert, davet_demand_prior, davet_denoise_step,
     davet_head_tiled_elems, davet_pack_head, davet_parse_operation,
     davet_policy_envelope, davet_policy_step, davet_policy_step_device,
     davet_realizer_key_count,

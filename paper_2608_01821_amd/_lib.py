@@ -87,6 +87,8 @@ _SIGS = {
     "davet_view_map_sizes": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
     "davet_build_views": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp, _P_vp,
                                     _P_vp, _vp, C.c_size_t, _vp]),
+    "davet_build_views_static": (C.c_int, [C.POINTER(ViewGeom), _vp, _P_vp,
+                                           _P_vp, _P_vp, _vp]),
     "davet_views_scratch_bytes": (C.c_int, [C.POINTER(ViewGeom),
                                             C.POINTER(C.c_size_t)]),
     "davet_realizer_key_count": (C.c_int, [C.POINTER(ViewGeom), _P_i32]),
@@ -254,6 +256,21 @@ def davet_build_views(geom, v, levels, offsets=None, members=None,
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
     _check(_L.davet_build_views(C.byref(geom), _ptr(v), lv, off, mem,
                                 _ptr(scratch), nbytes, _stream(stream)))
+
+
+STATIC_SCRATCH_BYTES = 4 << 20
+
+
+def davet_build_views_static(geom, v, levels, offsets=None, members=None,
+                             stream=None):
+    """davet_build_views with the library's own device scratch (no
+    allocation by the library or by this binding)."""
+    K = geom.K
+    lv = _ptr_array(list(levels) + [None] * (K - len(levels)))
+    off = _ptr_array(offsets) if offsets is not None else None
+    mem = _ptr_array(members) if members is not None else None
+    _check(_L.davet_build_views_static(C.byref(geom), _ptr(v), lv, off, mem,
+                                       _stream(stream)))
 
 
 def davet_realizer_key_count(geom):

@@ -17,6 +17,9 @@
 // are labelled and scattered by all lanes), and the level rows (CSR means,
 // float64 sums in member order, rounded once).
 
+#include <mutex>
+#include <string>
+
 #include "common.h"
 
 namespace davet {
@@ -601,4 +604,71 @@ extern "C" int davet_realizer_maps(const davet_view_geom* g,
     mp.mem[l] = idx_members ? idx_members[l] : nullptr;
   }
   return launch_maps(*g, keys, mp, stream);
+}
+
+// ---------------------------------------------------------------------------
+// davet_build_views_static: davet_build_views with the realizers' scratch
+// (keys and the index maps of the pooled levels) in a file-scope device
+// array instead of caller memory, for callers that cannot allocate.  Host
+// code never passes the array's name to a kernel (in host code it is only a
+// stand-in for the symbol): the device address is resolved once per device
+// with hipGetSymbolAddress and kept.  Every call on a device shares that
+// device's array; the keys and maps are written in full before they are
+// read, so nothing needs clearing, and calls that overlap on one device race.
+
+static __device__ __align__(256) char scratch[DAVET_STATIC_SCRATCH_BYTES];
+
+namespace davet {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (resolved on the first
+// call on that device).
+int static_scratch(void** out) {
+  int dev = -1;
+  DAVET_HIP(hipGetDevice(&dev));
+  DAVET_CHECK_ARG(dev >= 0 && dev < kMaxDevices, DAVET_EHIP,
+                  "davet_build_views_static: device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    DAVET_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    DAVET_CHECK_ARG(p != nullptr && ((uintptr_t)p & 255) == 0, DAVET_EHIP,
+                    "davet_build_views_static: scratch address unusable");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return DAVET_OK;
+}
+
+}  // namespace
+}  // namespace davet
+
+extern "C" int davet_build_views_static(const davet_view_geom* g,
+                                        const void* v, void* const* levels,
+                                        int32_t* const* idx_offsets,
+                                        int32_t* const* idx_members,
+                                        hipStream_t stream) {
+  using namespace davet;
+  DAVET_CHECK_ARG(g, DAVET_EINVAL, "davet_build_views_static: null geometry");
+  int rc = check_view_geom(g, "davet_build_views_static");
+  if (rc) return rc;
+  const size_t need = realizer_scratch_bytes(*g);
+  DAVET_CHECK_ARG(need <= DAVET_STATIC_SCRATCH_BYTES, DAVET_ENOMEM,
+                  "davet_build_views_static: the geometry needs " +
+                      std::to_string(need) + " bytes of scratch, more than "
+                      "the static maximum of " +
+                      std::to_string((size_t)DAVET_STATIC_SCRATCH_BYTES) +
+                      " (use davet_build_views with caller scratch)");
+  void* sc = nullptr;
+  if (need) {
+    rc = static_scratch(&sc);
+    if (rc) return rc;
+  }
+  return davet_build_views(g, v, levels, idx_offsets, idx_members, sc,
+                           need ? (size_t)DAVET_STATIC_SCRATCH_BYTES : 0,
+                           stream);
 }
