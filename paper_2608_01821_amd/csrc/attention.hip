@@ -22,8 +22,16 @@
 // 1/sqrt(D) scale).  The groups' partial (max, normaliser, O) are merged
 // through LDS at the end.  Ragged tails: keys past the sequence end score
 // -inf; queries past it are computed on clamped rows and never stored.
-// Workgroup ids are remapped so the query tiles of a head share an XCD (and
-// its L2 copy of that head's keys and values).
+// Workgroup ids are remapped so the full query tiles of a head share an XCD
+// (and its L2 copy of that head's keys and values); the ragged last tile of
+// each sequence (fewer than 128 queries) is dispatched after every full tile,
+// so that when the grid is slightly larger than one wave of workgroups the
+// work left for the second wave is the cheap part, and a wavefront whose 32
+// queries all lie past the sequence end only moves K/V and meets the
+// barriers.  The running maximum moves lazily: a lane adopts a new maximum
+// only when a score exceeds the current one by more than 2^8 in probability
+// (the probabilities, at most 2^8, stay well inside the 16-bit range and the
+// normaliser is an fp32 sum), so the O rescale is rare after the first tiles.
 
 #include "common.h"
 
@@ -50,6 +58,14 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 __device__ __forceinline__ int k_slot(int r, int c) { return c ^ (r & 15); }
 __device__ __forceinline__ int v_slot(int r, int c) { return c ^ ((r & 3) << 2); }
 
+// Workgroup barrier with no memory fence: each wave has waited for exactly
+// the loads it needs; the empty asm statements keep LDS accesses in place.
+__device__ __forceinline__ void sync_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ int remap_xcd_attn(int bid, int nwg) {
   const int full = nwg & ~7;
   if (bid >= full) return bid;
@@ -57,18 +73,33 @@ __device__ __forceinline__ int remap_xcd_attn(int bid, int nwg) {
   return (bid & 7) * per + (bid >> 3);
 }
 
-__device__ __forceinline__ void locate_tile(const SeqPack& sp, int tile,
+// Full query tile `tile` (in sequence order) -> sequence s and its tile qt.
+__device__ __forceinline__ void locate_full(const SeqPack& sp, int tile,
                                             int qtile, int& s, int& qt) {
   s = 0;
   int acc = 0;
   for (;;) {
-    const int n = sp.row0[s + 1] - sp.row0[s];
-    const int nt = (n + qtile - 1) / qtile;
+    const int nt = (sp.row0[s + 1] - sp.row0[s]) / qtile;
     if (tile < acc + nt || s + 1 >= sp.n_seqs) break;
     acc += nt;
     ++s;
   }
   qt = tile - acc;
+}
+// Ragged tile `r` -> the r-th sequence (in order) whose length is not a
+// multiple of qtile, and its last tile.
+__device__ __forceinline__ void locate_ragged(const SeqPack& sp, int r,
+                                              int qtile, int& s, int& qt) {
+  s = 0;
+  for (;;) {
+    const int n = sp.row0[s + 1] - sp.row0[s];
+    if (n % qtile) {
+      if (r == 0 || s + 1 >= sp.n_seqs) { qt = n / qtile; return; }
+      --r;
+    }
+    ++s;
+    if (s >= sp.n_seqs) { s = sp.n_seqs - 1; qt = 0; return; }
+  }
 }
 
 // One key group (enough workgroups for the chip), fp16: a single K/V buffer
@@ -89,7 +120,8 @@ constexpr int attn_minb() {
 template <typename Fmt, int SPLIT>
 __global__ void __launch_bounds__(256 * SPLIT, (attn_minb<Fmt, SPLIT>()))
 attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
-              SeqPack sp, int n_heads, int n_tiles, float scale_log2) {
+              SeqPack sp, int n_heads, int n_full, int n_ragged,
+              float scale_log2) {
   using v8 = typename Fmt::v8;
   // SPLIT groups' double-buffered K/V tiles; after the loop the same bytes
   // hold the merge (O as [4 waves][4][16][64 lanes] floats, then max and
@@ -100,10 +132,20 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   constexpr int LDS_U16 = SPLIT * GROUP_LDS > MERGE_U16 ? SPLIT * GROUP_LDS
                                                         : MERGE_U16;
   __shared__ __attribute__((aligned(1024))) uint16_t smem[LDS_U16];
-  const int logical = remap_xcd_attn(blockIdx.x, gridDim.x);
-  const int h = logical / n_tiles;
-  int s, qt;
-  locate_tile(sp, logical % n_tiles, QT, s, qt);
+  // blocks [0, n_heads * n_full): full tiles, head-major, XCD-remapped;
+  // then the ragged tiles, head-major
+  const int n_fb = n_heads * n_full;
+  int h, s, qt;
+  if ((int)blockIdx.x < n_fb) {
+    const int logical = remap_xcd_attn(blockIdx.x, n_fb);
+    h = logical / n_full;
+    locate_full(sp, logical % n_full, QT, s, qt);
+  } else {
+    const int r = blockIdx.x - n_fb;
+    const int nr = max(n_ragged, 1);
+    h = r / nr;
+    locate_ragged(sp, r % nr, QT, s, qt);
+  }
   const int d = n_heads * HD;
   const size_t ld = (size_t)3 * d;
   const int row0 = sp.row0[s];
@@ -115,6 +157,8 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   const int l32 = lane & 31, hh = lane >> 5;
   const int q = qt * QT + wave * 32 + l32;
   const int qc = min(q, N - 1);
+  // a wavefront whose queries all lie past the sequence end only moves K/V
+  const bool live = qt * QT + wave * 32 < N;
   char* gbuf = reinterpret_cast<char*>(smem + grp * GROUP_LDS);
 
   // Q^T fragments (B operand): 8 k-steps of 16 head dims
@@ -149,118 +193,142 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       dma16(vbase + go + v_slot(r, lane & 15) * 8, vd + (wave * 4 + qi) * 1024);
     }
   };
-
   const int n_kt = (N + KT - 1) / KT;
   const int n_it = (n_kt + SPLIT - 1) / SPLIT;     // same for every group
-  if (grp < n_kt) issue(grp, 0);
-  for (int it = 0; it < n_it; ++it) {
-    const int kb = it * SPLIT + grp;
-    const bool have = kb < n_kt;
-    // this wave's loads of tile kb have landed (and, with two buffers, its
-    // reads of the other one are done); after the barrier, so are every wave's
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if constexpr (BUFS == 2)
-      if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
-    if (have) {
-      const char* Kb = gbuf + (BUFS == 2 ? (it & 1) : 0) * (BUF_U16 * 2);
-      const char* Vb = Kb + TILE_U16 * 2;
-      const int k0 = kb * KT;
-      // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
-      f32x16 sc[2];
+
+  // the three parts of a key tile's work, on the K and V of one buffer
+  auto qk_scores = [&](const char* Kb, f32x16 (&sc)[2]) {
+    // ---- S^T = K Q^T for 64 keys x 32 queries (two 32-key halves)
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
+    for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
-        const int r = mt * 32 + l32;
+      for (int e = 0; e < 16; ++e) sc[mt][e] = 0.f;
+      const int r = mt * 32 + l32;
 #pragma unroll
-        for (int ks = 0; ks < HD / 16; ++ks) {
-          const v8 kf = *reinterpret_cast<const v8*>(
-              Kb + r * 256 + (k_slot(r, ks * 2 + hh) << 4));
-          sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
-        }
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        const v8 kf = *reinterpret_cast<const v8*>(
+            Kb + r * 256 + (k_slot(r, ks * 2 + hh) << 4));
+        sc[mt] = Fmt::mfma32(kf, qf[ks], sc[mt]);
       }
-      // ---- online softmax for this lane's query over its 32 keys + partner's.
-      // The running max is kept on raw scores (the scale is positive), so
-      // each probability costs one fma and one exp2: 2^(s*scale - m*scale).
-      if (k0 + KT > N) {                 // ragged last tile only
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = k0 + mt * 32 + (e >> 2) * 8 + hh * 4 + (e & 3);
-            if (key >= N) sc[mt][e] = -INFINITY;
-          }
-      }
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sc[mt][e]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float m_new = fmaxf(m_run, tmax);
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
-      const float neg_m = -m_new * scale_log2;
-      float psum = 0.f;
-      uint16_t pb[4][8];
+    }
+  };
+  auto softmax = [&](int k0, f32x16 (&sc)[2], uint32_t (&pw2)[4][4]) {
+    // ---- online softmax for this lane's query over its 32 keys + partner's.
+    // The running max is kept on raw scores (the scale is positive), so
+    // each probability costs one fma and one exp2: 2^(s*scale - m*scale).
+    if (k0 + KT > N) {                 // ragged last tile only
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[mt][e], scale_log2, neg_m));
-          psum += p;
-          pb[mt * 2 + (e >> 3)][e & 7] = Fmt::store(p);
+          const int key = k0 + mt * 32 + (e >> 2) * 8 + hh * 4 + (e & 3);
+          if (key >= N) sc[mt][e] = -INFINITY;
         }
-      psum += __shfl_xor(psum, 32, 64);
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
-      // rescale the accumulator unless no lane's maximum moved
-      if (__any(alpha != 1.0f)) {
+    }
+    float tmax = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < HD / 32; ++i)
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sc[mt][e]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    // lazy maximum: keep m_run unless a score exceeds it by more than
+    // 8 / scale_log2 (probabilities up to 2^8); the first tile always moves
+    const float m_new =
+        (tmax - m_run) * scale_log2 > 8.0f ? tmax : m_run;
+    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
+    const float neg_m = -m_new * scale_log2;
+    float psum = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[mt][e], scale_log2, neg_m));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[mt][e + 1], scale_log2, neg_m));
+        psum += p0;
+        psum += p1;
+        pw2[mt * 2 + (e >> 3)][(e & 7) >> 1] = Fmt::store2(p0, p1);
       }
-      // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    // rescale the accumulator unless no lane's maximum moved
+    if (__any(alpha != 1.0f)) {
 #pragma unroll
-      for (int ps = 0; ps < 4; ++ps) {
+      for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
-        for (int dt = 0; dt < HD / 32; ++dt) {
-          // V^T fragment by transposing reads of the row-major tile: within
-          // each 16-lane group, lane i receives element i % 4 of the 8-byte
-          // piece addressed by group lane 4r + i / 4, for r = 0..3; group
-          // lane j therefore addresses key ks + 4*(lane / 32) + j / 4 and dims
-          // dt*32 + 16*((lane / 16) & 1) + 4*(j % 4), so lane l collects keys
-          // ks + 4*(l / 32) + r of dim dt*32 + l % 32 (ks = ps*16, +8 for the
-          // second half of the fragment); an 8-byte piece never crosses a
-          // 16-byte chunk, so the swizzle moves it whole
-          const int j = lane & 15;
-          const int r = ps * 16 + hh * 4 + (j >> 2);
-          const int dd = dt * 32 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
-          const char* vp = Vb + r * 256 + (v_slot(r, dd >> 3) << 4) + (dd & 7) * 2;
-          const v4s t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_ptr)vp);
-          const v4s t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4s_ptr)(vp + 8 * 256));
-          const u32x2 v0 = __builtin_bit_cast(u32x2, t0);
-          const u32x2 v1 = __builtin_bit_cast(u32x2, t1);
-          u32x4 vv;
-          vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
-          u32x4 pw;
+        for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+    }
+  };
+  auto pv_accumulate = [&](const char* Vb, const uint32_t (&pw2)[4][4]) {
+    // ---- O^T += V^T P^T: k-step ps covers keys 16*ps .. 16*ps+15
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            pw[u] = (uint32_t)pb[ps][2 * u] | ((uint32_t)pb[ps][2 * u + 1] << 16);
-          o[dt] = Fmt::mfma32(__builtin_bit_cast(v8, vv),
-                              __builtin_bit_cast(v8, pw), o[dt]);
-        }
+    for (int ps = 0; ps < 4; ++ps) {
+#pragma unroll
+      for (int dt = 0; dt < HD / 32; ++dt) {
+        // V^T fragment by transposing reads of the row-major tile: within
+        // each 16-lane group, lane i receives element i % 4 of the 8-byte
+        // piece addressed by group lane 4r + i / 4, for r = 0..3; group
+        // lane j therefore addresses key ks + 4*(lane / 32) + j / 4 and dims
+        // dt*32 + 16*((lane / 16) & 1) + 4*(j % 4), so lane l collects keys
+        // ks + 4*(l / 32) + r of dim dt*32 + l % 32 (ks = ps*16, +8 for the
+        // second half of the fragment); an 8-byte piece never crosses a
+        // 16-byte chunk, so the swizzle moves it whole
+        const int j = lane & 15;
+        const int r = ps * 16 + hh * 4 + (j >> 2);
+        const int dd = dt * 32 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+        const char* vp = Vb + r * 256 + (v_slot(r, dd >> 3) << 4) + (dd & 7) * 2;
+        const v4s t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_ptr)vp);
+        const v4s t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4s_ptr)(vp + 8 * 256));
+        const u32x2 v0 = __builtin_bit_cast(u32x2, t0);
+        const u32x2 v1 = __builtin_bit_cast(u32x2, t1);
+        u32x4 vv;
+        vv[0] = v0[0]; vv[1] = v0[1]; vv[2] = v1[0]; vv[3] = v1[1];
+        u32x4 pw;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) pw[u] = pw2[ps][u];
+        o[dt] = Fmt::mfma32(__builtin_bit_cast(v8, vv),
+                            __builtin_bit_cast(v8, pw), o[dt]);
       }
     }
-    if constexpr (BUFS == 1) {
-      // every wave is done reading the buffer: refill it
+  };
+
+  if constexpr (BUFS == 1) {
+    // one buffer, refilled once every wave is done with it (the other
+    // workgroups on the CU hide the load)
+    if (n_kt > 0) issue(0, 0);
+    for (int kb = 0; kb < n_kt; ++kb) {
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      sync_lds();
+      if (live) {
+        f32x16 sc[2];
+        qk_scores(gbuf, sc);
+        uint32_t pw2[4][4];
+        softmax(kb * KT, sc, pw2);
+        pv_accumulate(gbuf + TILE_U16 * 2, pw2);
+      }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __builtin_amdgcn_s_barrier();
-      asm volatile("" ::: "memory");
-      if (kb + SPLIT < n_kt) issue(kb + SPLIT, 0);
+      sync_lds();
+      if (kb + 1 < n_kt) issue(kb + 1, 0);
+    }
+  } else {
+    if (grp < n_kt) issue(grp, 0);
+    for (int it = 0; it < n_it; ++it) {
+      const int kb = it * SPLIT + grp;
+      const bool have = kb < n_kt && live;
+      // this wave's loads of tile kb have landed, and its reads of the other
+      // buffer are done; after the barrier, so are every wave's
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      sync_lds();
+      if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
+      if (have) {
+        const char* Kb = gbuf + (it & 1) * (BUF_U16 * 2);
+        f32x16 sc[2];
+        qk_scores(Kb, sc);
+        uint32_t pw2[4][4];
+        softmax(kb * KT, sc, pw2);
+        pv_accumulate(Kb + TILE_U16 * 2, pw2);
+      }
     }
   }
 
@@ -356,9 +424,13 @@ int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
                        hipStream_t s) {
   if (head_dim != HD)
     return set_error(DAVET_ESHAPE, "attention16: head_dim must be 128");
-  int tiles = 0;
-  for (int i = 0; i < sp.n_seqs; ++i)
-    tiles += (sp.row0[i + 1] - sp.row0[i] + QT - 1) / QT;
+  int n_full = 0, n_ragged = 0;
+  for (int i = 0; i < sp.n_seqs; ++i) {
+    const int n = sp.row0[i + 1] - sp.row0[i];
+    n_full += n / QT;
+    n_ragged += n % QT != 0;
+  }
+  const int tiles = n_full + n_ragged;
   if (tiles == 0) return DAVET_OK;
   ProfScope ps(KC_ATTN, s);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
@@ -373,10 +445,10 @@ int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
 #define ATTN(F)                                                                \
   if (split)                                                                   \
     hipLaunchKernelGGL((attn16_kernel<F, 2>), grid, dim3(512), 0, s, qkv, o,   \
-                       sp, n_heads, tiles, scale_log2);                        \
+                       sp, n_heads, n_full, n_ragged, scale_log2);             \
   else                                                                         \
     hipLaunchKernelGGL((attn16_kernel<F, 1>), grid, dim3(256), 0, s, qkv, o,   \
-                       sp, n_heads, tiles, scale_log2)
+                       sp, n_heads, n_full, n_ragged, scale_log2)
   if (dtype == DAVET_F16) { ATTN(F16); } else { ATTN(BF16); }
 #undef ATTN
   DAVET_HIP(hipGetLastError());

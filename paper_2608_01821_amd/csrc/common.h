@@ -95,6 +95,10 @@ struct BF16 {
   static constexpr int dtype = DAVET_BF16;
   __device__ static __forceinline__ float load(uint16_t b) { return bf16_to_f32(b); }
   __device__ static __forceinline__ uint16_t store(float f) { return f32_to_bf16(f); }
+  // two values rounded (nearest even) into one word, a in the low half
+  __device__ static __forceinline__ uint32_t store2(float a, float b) {
+    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+  }
   __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_bf16(x); }
   __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -105,6 +109,14 @@ struct F16 {
   static constexpr int dtype = DAVET_F16;
   __device__ static __forceinline__ float load(uint16_t h) { return f16_to_f32(h); }
   __device__ static __forceinline__ uint16_t store(float f) { return f32_to_f16(f); }
+  // two values rounded (nearest even) into one word, a in the low half: one
+  // packed conversion (v_cvt_pk_f16_f32) instead of two and a merge
+  __device__ static __forceinline__ uint32_t store2(float a, float b) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const f2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
+  }
   __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_f16(x); }
   __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
