@@ -4,7 +4,9 @@
 // window's tokens once, in row-major order, adding each into the running
 // float64 sum of the sub-window it belongs to at every finer level.  Each
 // level token is then (sum / member count) rounded once to the view dtype.
-// HBM-bound: v is read once, the levels are written once.
+// HBM-bound: v is read once, the levels are written once.  Every token of a
+// thread's window is loaded before any is summed, so a thread has the whole
+// window in flight.
 //
 // Mixed view (K = 3, stride S): level 1 becomes, per crop, the level-0 tokens
 // followed by the raw tokens on the lattice (o + aS, o + bS), o = S/2.  The
@@ -49,38 +51,60 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
     for (int e = 0; e < VEC; ++e) acc[a][e] = 0.0;
 
   const int r0 = I * F, s0 = J * F;
+  // Every token of the window is loaded before any is summed (F*F loads in
+  // flight per thread instead of one memory round trip per token); tokens
+  // past the grid edge load a clamped in-bounds row and add +0.0, an exact
+  // no-op on a sum that starts at +0.0, so the sums are the member sums in
+  // member order bit for bit.
+  constexpr int WORDS = VEC * (int)sizeof(T) / 4;   // 32-bit words per load
+  uint32_t raw[F * F][WORDS];
+#pragma unroll
+  for (int dr = 0; dr < F; ++dr) {
+#pragma unroll
+    for (int ds = 0; ds < F; ++ds) {
+      const int r = min(r0 + dr, G - 1), s = min(s0 + ds, G - 1);
+      const T* src = v + ((size_t)c * G * G + (size_t)r * G + s) * d + e0;
+      if constexpr (WORDS % 4 == 0) {
+#pragma unroll
+        for (int q4 = 0; q4 < WORDS / 4; ++q4) {
+          const u32x4 w = reinterpret_cast<const u32x4*>(src)[q4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) raw[dr * F + ds][q4 * 4 + q] = w[q];
+        }
+      } else if constexpr (WORDS == 2) {
+        const u32x2 w = *reinterpret_cast<const u32x2*>(src);
+        raw[dr * F + ds][0] = w[0];
+        raw[dr * F + ds][1] = w[1];
+      } else {
+        static_assert(WORDS == 1, "load width");
+        raw[dr * F + ds][0] = *reinterpret_cast<const uint32_t*>(src);
+      }
+    }
+  }
   // Fully unrolled so every accumulator index is a compile-time constant.
 #pragma unroll
   for (int dr = 0; dr < F; ++dr) {
 #pragma unroll
     for (int ds = 0; ds < F; ++ds) {
       const int r = r0 + dr, s = s0 + ds;
-      if (r >= G || s >= G) continue;
+      const bool inb = r < G && s < G;
       const T* src = v + ((size_t)c * G * G + (size_t)r * G + s) * d + e0;
-      float x[VEC];
+      double x[VEC];
       if constexpr (sizeof(T) == 2) {
-        if constexpr (VEC == 8) {
-          u32x4 w = *reinterpret_cast<const u32x4*>(src);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            x[2 * q] = Fmt::load((uint16_t)(w[q] & 0xffffu));
-            x[2 * q + 1] = Fmt::load((uint16_t)(w[q] >> 16));
-          }
-        } else {
-          uint32_t w = *reinterpret_cast<const uint32_t*>(src);
-          x[0] = Fmt::load((uint16_t)(w & 0xffffu));
-          x[1] = Fmt::load((uint16_t)(w >> 16));
+        for (int q = 0; q < VEC / 2; ++q) {
+          const uint32_t w = raw[dr * F + ds][q];
+          x[2 * q] = inb ? (double)Fmt::load((uint16_t)(w & 0xffffu)) : 0.0;
+          x[2 * q + 1] = inb ? (double)Fmt::load((uint16_t)(w >> 16)) : 0.0;
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < VEC; e += 2) {
-          float2 w = *reinterpret_cast<const float2*>(src + e);
-          x[e] = w.x; x[e + 1] = w.y;
-        }
+        for (int e = 0; e < VEC; ++e)
+          x[e] = inb ? (double)__uint_as_float(raw[dr * F + ds][e]) : 0.0;
       }
       if constexpr (MIXED) {
         const int o = S / 2;
-        if (r % S == o && s % S == o) {           // lattice token: copy bits
+        if (inb && r % S == o && s % S == o) {    // lattice token: copy bits
           const int m = lattice_len(G, S);
           const size_t tok = (size_t)c * (Wc * Wc + m * m) + Wc * Wc +
                              (size_t)(r / S) * m + (s / S);
@@ -96,7 +120,7 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
         const int per = F / f;                     // sub-windows per side
         const int a = base + (dr / f) * per + (ds / f);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[a][e] += (double)x[e];
+        for (int e = 0; e < VEC; ++e) acc[a][e] += x[e];
         base += per * per;
       }
     }
@@ -140,7 +164,16 @@ pool_views_kernel(const typename Fmt::st* __restrict__ v, LevelOut out,
             if constexpr (MIXED)
               *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out.p[1]) +
                                         tok_mix * d + e0) = w;
+          } else if constexpr (VEC == 4) {
+            u32x2 w;
+            w[0] = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+            w[1] = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+            *reinterpret_cast<u32x2*>(dst) = w;
+            if constexpr (MIXED)
+              *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(out.p[1]) +
+                                        tok_mix * d + e0) = w;
           } else {
+            static_assert(VEC == 2, "store width");
             const uint32_t w = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
             *reinterpret_cast<uint32_t*>(dst) = w;
             if constexpr (MIXED)
@@ -224,7 +257,7 @@ void launch_pool_k(const davet_view_geom& g, const void* v, const LevelOut& lo,
     case 2: launch_pool<2, 8, Fmt>(g, v, lo, s); break;
     case 3:
       if (g.mixed_stride > 0) launch_pool<3, 8, Fmt, true>(g, v, lo, s);
-      else launch_pool<3, 8, Fmt>(g, v, lo, s);
+      else launch_pool<3, 4, Fmt>(g, v, lo, s);
       break;
     default: launch_pool<4, 2, Fmt>(g, v, lo, s); break;
   }
