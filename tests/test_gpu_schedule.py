@@ -67,7 +67,8 @@ def test_teacher_forced_loop(cid):
         assert np.array_equal(d_m.cpu().numpy(), masked)
 
 
-def _run_schedule(cfg, mdl, s, pols=None, fixed=None, weights=None):
+def _run_schedule(cfg, mdl, s, pols=None, fixed=None, weights=None,
+                  mailbox=None):
     n = cfg.n_seqs
     L, T = cfg.resp_len, cfg.steps
     mode = mdl.mode
@@ -88,7 +89,7 @@ def _run_schedule(cfg, mdl, s, pols=None, fixed=None, weights=None):
     levels, budgets = dv.davet_run_schedule(
         model_cfg(cfg, mode), weights or mdl.weights, geoms, visual, bufs,
         prompt, cu, L, T,
-        cfg.k, pols, fixed, ids, msk, ws, ctr, atr)
+        cfg.k, pols, fixed, ids, msk, ws, ctr, atr, mailbox=mailbox)
     torch.cuda.synchronize()
     return (np.array(levels).reshape(n, T), np.array(budgets).reshape(n, T),
             ctr.cpu().numpy().reshape(T, n, L),
@@ -311,3 +312,36 @@ def test_run_schedule_64_sequences():
         assert ref["trace"]["levels"][0] == lv[i, 0]
         assert _trajectory_prefix_match(cfg, ref["trace"], ctr, atr, msk,
                                         i) >= 1
+
+
+def test_run_schedule_wait_limit_and_mailbox_reuse():
+    """The host's wait for a step's published levels is bounded: with a
+    limit far below one step's duration (one 8B-shaped layer, ~0.5 ms per
+    step) the call returns DAVET_EHIP while the stream keeps running, and
+    after the stream drains the same mailbox serves a normal call whose
+    levels and budgets equal those of a call on a fresh mailbox (each call
+    takes stamps no earlier call on that mailbox used)."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_config(2), steps=3, schedule="policy",
+                              fixed_levels=None)
+    mdl = Model(cfg, keep_host=False)
+    s = synth.gen_sample(cfg)
+    p = cfg.policy
+    pols = [dv.Policy(p["B"], p["rho"], p["alpha"], dv.davet_demand_prior(0),
+                      1 if p["early"] else 0, cfg.K)]
+    mb = dv.Mailbox()
+    try:
+        dv.davet_set_wait_limit(1e-6)
+        with pytest.raises(dv.DavetError) as e:
+            _run_schedule(cfg, mdl, s, pols=pols, mailbox=mb)
+        assert e.value.status == -5 and "no levels published" in str(e.value)
+    finally:
+        torch.cuda.synchronize()          # the failed call's steps drain
+        dv.davet_set_wait_limit(120.0)
+    lv_a, bu_a = _run_schedule(cfg, mdl, s, pols=pols, mailbox=mb)[:2]
+    mb2 = dv.Mailbox()
+    lv_b, bu_b = _run_schedule(cfg, mdl, s, pols=pols, mailbox=mb2)[:2]
+    mb.close()
+    mb2.close()
+    assert np.array_equal(lv_a, lv_b) and np.array_equal(bu_a, bu_b)
+    assert np.all(np.isfinite(bu_a))
