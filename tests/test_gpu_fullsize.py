@@ -75,7 +75,7 @@ def check_sampled(cfg, mdl, sample, level, ids, masked, g_conf, g_am,
     assert err <= tol["logits"], ("logits rel-RMS", err)
     gap = 6.0 * err * float(np.sqrt(np.mean(lg ** 2)))
     check_decode(g_am[pos], g_conf[pos], lg, am, cf, cfg.mask_id, gap,
-                 tol["conf"])
+                 g_lg[pos])
     say("  rel-RMS %.3e" % err)
     return err
 

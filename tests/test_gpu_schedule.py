@@ -144,6 +144,13 @@ def _oracle_states(cfg, tr):
     return out
 
 
+# The free-running loop stores no logits, so the per-row confidence bound of
+# the teacher-forced checks (derived from the logit error) is not available
+# here; along the shared prefix of the two trajectories a coarse relative
+# tolerance is used instead (the tight checks are the teacher-forced ones).
+TRAJ_CONF_RTOL = {"f32": 1e-4, "bf16": 5e-2}
+
+
 def _trajectory_prefix_match(cfg, ref_tr, conf_tr, am_tr, final_masked, s):
     """Steps compared while the GPU and oracle states coincide; returns the
     number of steps compared."""
@@ -156,8 +163,7 @@ def _trajectory_prefix_match(cfg, ref_tr, conf_tr, am_tr, final_masked, s):
         c = conf_tr[t, s][gl]
         r = ref_tr["conf"][t][ol]
         err = np.abs(c - r) / r
-        assert err.max() <= TOL["f32" if cfg.dtype == "f32" else "f16"][
-            "conf"], (t, err.max())
+        assert err.max() <= TRAJ_CONF_RTOL[cfg.dtype], (t, err.max())
         n_ok += 1
     return n_ok
 
