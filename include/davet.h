@@ -26,7 +26,8 @@
  *   - Device work is enqueued asynchronously on the given HIP stream.  Only
  *     davet_run_schedule in policy mode synchronises: once per step, on the
  *     GPU kernel that writes the next levels (the next step's launch sizes
- *     depend on them).
+ *     depend on them); and davet_fp16_overflow_count, which reads a counter
+ *     back to the host.
  *   - Every argument is validated before anything is enqueued; on an error the
  *     call returns a negative davet_status, enqueues nothing, and
  *     davet_last_error() describes the failure (thread-local string).
@@ -338,6 +339,24 @@ int davet_denoise_step(const davet_model_cfg* cfg, const davet_weights* w,
                        const uint8_t* resp_masked, int32_t L, float* conf_out,
                        int32_t* argmax_out, float* logits_out, void* workspace,
                        size_t ws_bytes, hipStream_t stream);
+
+/* Number of non-finite values the 16-bit modes stored as GEMM outputs in the
+ * last davet_denoise_step on this workspace, or over all the steps of the
+ * last davet_run_schedule on it.  The counted stores are the projections'
+ * 16-bit outputs: Q/K/V (after rotary embedding) and the SwiGLU product fed
+ * to the down projection.  In DAVET_F16 a value beyond +-65504 becomes +-inf
+ * there, so a nonzero count means the fp16 range was too small for this model
+ * and input (run it in DAVET_F32, or DAVET_BF16 for a shallow stack).  The
+ * other 16-bit tensors are bounded by these or by a norm: attention outputs
+ * are convex combinations of V rows, and normed rows are at most
+ * sqrt(d) * max|gain| in magnitude.  The residual stream and the logits are
+ * float32 and not counted; a DAVET_F32 model always reads 0.
+ *   workspace: the same 256-byte aligned workspace the step ran on (the
+ *   counter is its first 4 bytes); count: HOST int32.
+ * Enqueues a 4-byte read on `stream` and waits for it.  Errors: EINVAL (null
+ * or misaligned pointer), EHIP (the copy or the wait failed). */
+int davet_fp16_overflow_count(const void* workspace, int32_t* count /*host*/,
+                              hipStream_t stream);
 
 /* --------------------------------------------------------------- unmask -- */
 

@@ -62,21 +62,33 @@ def _f64(w):
     return np.asarray(w, dtype=np.float64)
 
 
-def layer(x: np.ndarray, w: dict, n_heads: int, head_dim: int, eps: float,
-          ang: np.ndarray) -> np.ndarray:
+def layer_parts(x: np.ndarray, w: dict, n_heads: int, head_dim: int,
+                eps: float, ang: np.ndarray):
     """One pre-norm layer: x + O(attn(rope(q), rope(k), v)) then
-    x + down(silu(gate a) * up a), with a = RMSNorm of the running x."""
+    x + down(silu(gate a) * up a), with a = RMSNorm of the running x.
+
+    Returns (output, qkv, hdn): the layer output, the projected
+    [q | k | v] columns with the rotary embedding applied to q and k, and
+    the SwiGLU product fed to the down projection."""
     N, d = x.shape
     a = rmsnorm(x, w.get("attn_norm"), eps)
     qkv = a @ _f64(w["wqkv"]).T
-    q = qkv[:, :d].reshape(N, n_heads, head_dim)
-    k = qkv[:, d:2 * d].reshape(N, n_heads, head_dim)
+    q = rope(qkv[:, :d].reshape(N, n_heads, head_dim), ang)
+    k = rope(qkv[:, d:2 * d].reshape(N, n_heads, head_dim), ang)
     v = qkv[:, 2 * d:].reshape(N, n_heads, head_dim)
-    o = attention(rope(q, ang), rope(k, ang), v).reshape(N, d)
+    o = attention(q, k, v).reshape(N, d)
     x = x + o @ _f64(w["wo"]).T
     a = rmsnorm(x, w.get("ffn_norm"), eps)
     hdn = silu(a @ _f64(w["wg"]).T) * (a @ _f64(w["wu"]).T)
-    return x + hdn @ _f64(w["wd"]).T
+    qkv_rot = np.concatenate([q.reshape(N, d), k.reshape(N, d),
+                              v.reshape(N, d)], axis=1)
+    return x + hdn @ _f64(w["wd"]).T, qkv_rot, hdn
+
+
+def layer(x: np.ndarray, w: dict, n_heads: int, head_dim: int, eps: float,
+          ang: np.ndarray) -> np.ndarray:
+    """One pre-norm layer (the output of layer_parts)."""
+    return layer_parts(x, w, n_heads, head_dim, eps, ang)[0]
 
 
 def embed_sequence(view, prompt_ids, resp_ids, masked, embed, mask_id):

@@ -104,6 +104,7 @@ _SIGS = {
                                      _i32, _P_vp, _P_i32, _vp, _P_i32, _vp,
                                      _vp, _i32, _vp, _vp, _vp, _vp, C.c_size_t,
                                      _vp]),
+    "davet_fp16_overflow_count": (C.c_int, [_vp, _P_i32, _vp]),
     "davet_unmask": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
                                _vp]),
     "davet_demand_prior": (C.c_double, [_i32]),
@@ -326,6 +327,15 @@ def davet_denoise_step(cfg, weights: Weights, views, n_view, prompt_ids,
         _ptr(resp_ids), _ptr(resp_masked), int(L), _ptr(conf_out),
         _ptr(argmax_out), _ptr(logits_out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def davet_fp16_overflow_count(workspace, stream=None) -> int:
+    """Non-finite 16-bit projection outputs stored by the last step (or
+    schedule) that ran on `workspace`; waits for `stream`."""
+    out = C.c_int32(0)
+    _check(_L.davet_fp16_overflow_count(_ptr(workspace), C.byref(out),
+                                        _stream(stream)))
+    return out.value
 
 
 def davet_unmask(n_seqs, L, k, conf, argmax, resp_ids, resp_masked,

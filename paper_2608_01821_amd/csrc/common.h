@@ -100,6 +100,10 @@ struct BF16 {
     return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
   }
   __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_bf16(x); }
+  // 1 when a stored value is not finite (all exponent bits set)
+  __device__ static __forceinline__ int nonfinite(uint16_t h) {
+    return (h & 0x7f80u) == 0x7f80u;
+  }
   __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
@@ -118,6 +122,11 @@ struct F16 {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
   }
   __device__ static __forceinline__ uint16_t from_f64(double x) { return f64_to_f16(x); }
+  // 1 when a stored value is not finite: for fp16 a result above 65504 in
+  // magnitude (after rounding) became +-inf
+  __device__ static __forceinline__ int nonfinite(uint16_t h) {
+    return (h & 0x7c00u) == 0x7c00u;
+  }
   __device__ static __forceinline__ f32x16 mfma32(v8 a, v8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
@@ -187,6 +196,8 @@ struct RowList {
   float* conf;
   int32_t* argmax;
   int32_t* slot;
+  int32_t* overflow;      // the step's 16-bit overflow counter (may be null)
+  int clear_overflow;     // the list builder zeroes it first
 };
 // assembly + first norm of every packed row; one extra workgroup builds the
 // masked-row list alongside
@@ -227,11 +238,13 @@ GemmPlan plan_gemm16(int M, int N, int K);
 // columns < rope_cols using pos[row] and the cos/sin table cs when pos is
 // given.  With plan.ksplit > 1 the kernel writes fp32 partials to `partials`
 // and the caller runs the matching reduce kernel below.
+// overflow (may be null): every 16-bit value the EPI_STORE / EPI_SWIGLU
+// epilogue stores as non-finite adds 1 to *overflow.
 int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
                   const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
                   int K, int ldc, const int32_t* pos, const float* cs,
                   int rope_cols, float* partials, size_t partial_cap, int cls,
-                  hipStream_t s);
+                  hipStream_t s, int32_t* overflow = nullptr);
 // Largest fp32 split-K partial buffer (bytes) plan_gemm16 may ask for with
 // M <= max_M rows of an N x K product.
 size_t gemm16_partial_bound(int max_M, int N, int K);
@@ -249,10 +262,12 @@ int launch_reduce_add_gather(int dtype, const float* P, int ksplit, int rows,
 //   out16[r][c] = rope(sum_s P[s][r][c]) for c < rope_cols, plain otherwise
 int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
                              int ncols, int rope_cols, const int32_t* pos,
-                             const float* cs, void* out, hipStream_t s);
+                             const float* cs, void* out, hipStream_t s,
+                             int32_t* overflow = nullptr);
 //   out16[r][c] = silu(sum_s P[s][r][c]) * sum_s P[s][r][F + c]
 int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
-                         int ffn, void* out, hipStream_t s);
+                         int ffn, void* out, hipStream_t s,
+                         int32_t* overflow = nullptr);
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,

@@ -83,6 +83,8 @@ struct EpiArgs {
   // step kt reads BK columns of each of its BN / 128 blocks in chunk
   // kt * BK / 64, from column kt * BK % 64.
   int b_tiled;
+  // non-finite 16-bit values stored by EPI_STORE / EPI_SWIGLU (may be null)
+  int32_t* overflow;
 };
 
 __device__ __forceinline__ int remap_xcd(int bid, int nwg) {
@@ -316,6 +318,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   // acc[i][j][e]: row = wm*WROWS + i*32 + (e/4)*8 + (lane/32)*4 + e%4,
   //               col = j*64 + wn*32 + lane%32   (tile-local)
   const int hrow = hh * 4;
+  int nf = 0;     // non-finite 16-bit values stored by this lane
   if constexpr (EPI == EPI_STORE) {
     uint16_t* C = reinterpret_cast<uint16_t*>(ep.C);
     const bool rope = ep.pos && n0 < ep.rope_cols;
@@ -332,12 +335,19 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
           for (int j = 0; j < TN; j += 2) {
             const float x = acc[i][j][e], y = acc[i][j + 1][e];
-            crow[j * 64] = Fmt::store(x * c.x - y * c.y);
-            crow[(j + 1) * 64] = Fmt::store(y * c.x + x * c.y);
+            const uint16_t a = Fmt::store(x * c.x - y * c.y);
+            const uint16_t b = Fmt::store(y * c.x + x * c.y);
+            nf += Fmt::nonfinite(a) + Fmt::nonfinite(b);
+            crow[j * 64] = a;
+            crow[(j + 1) * 64] = b;
           }
         } else {
 #pragma unroll
-          for (int j = 0; j < TN; ++j) crow[j * 64] = Fmt::store(acc[i][j][e]);
+          for (int j = 0; j < TN; ++j) {
+            const uint16_t a = Fmt::store(acc[i][j][e]);
+            nf += Fmt::nonfinite(a);
+            crow[j * 64] = a;
+          }
         }
       }
   } else if constexpr (EPI == EPI_ADD_F32) {
@@ -364,7 +374,9 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
         for (int j = 0; j < TN / 2; ++j) {
           const float g = acc[i][j][e], u = acc[i][j + TN / 2][e];
-          crow[j * 64] = Fmt::store(g / (1.0f + __expf(-g)) * u);
+          const uint16_t h = Fmt::store(g / (1.0f + __expf(-g)) * u);
+          nf += Fmt::nonfinite(h);
+          crow[j * 64] = h;
         }
       }
   } else if constexpr (EPI == EPI_PARTIAL) {
@@ -450,6 +462,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       ep.parg[o] = a;
     }
   }
+  if (nf && ep.overflow) atomicAdd(ep.overflow, nf);
   }  // M tiles
 }
 
@@ -644,7 +657,7 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
                   const uint16_t* B, const uint16_t* B2, void* C, int M, int N,
                   int K, int ldc, const int32_t* pos, const float* cs,
                   int rope_cols, float* partials, size_t partial_cap, int cls,
-                  hipStream_t s) {
+                  hipStream_t s, int32_t* overflow) {
   if (M <= 0) return DAVET_OK;
   if (plan.ksplit > 1 && (size_t)plan.ksplit * M * N * 4 > partial_cap)
     return set_error(DAVET_ENOMEM, "gemm16: split-K partials exceed the workspace");
@@ -665,6 +678,7 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
   ep.dual = epi == EPI_SWIGLU;
   ep.ffn = N / 2;
   ep.krot = plan.krot;
+  ep.overflow = overflow;
   return dtype == DAVET_F16
              ? gemm_dispatch<F16>(plan, epi, A, B, B2, M, N, K, ep, s)
              : gemm_dispatch<BF16>(plan, epi, A, B, B2, M, N, K, ep, s);

@@ -68,6 +68,22 @@ __device__ __forceinline__ void store8(typename Fmt::st* p, const float* v) {
   }
 }
 
+// store8 for 16-bit formats that also counts the non-finite values stored
+template <typename Fmt>
+__device__ __forceinline__ int store8_count(typename Fmt::st* p,
+                                            const float* v) {
+  u32x4 w;
+  int nf = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint16_t a = Fmt::store(v[2 * i]), b = Fmt::store(v[2 * i + 1]);
+    nf += Fmt::nonfinite(a) + Fmt::nonfinite(b);
+    w[i] = (uint32_t)a | ((uint32_t)b << 16);
+  }
+  *reinterpret_cast<u32x4*>(p) = w;
+  return nf;
+}
+
 __device__ __forceinline__ void load8f(const float* p, float* v) {
   load8<F32S>(p, v);
 }
@@ -136,7 +152,10 @@ __device__ __forceinline__ void build_row_list(const RowList& rl,
     if (i < w) base += wsum[i];
     all += wsum[i];
   }
-  if (threadIdx.x == 0) rl.list[0] = all;
+  if (threadIdx.x == 0) {
+    rl.list[0] = all;
+    if (rl.overflow && rl.clear_overflow) *rl.overflow = 0;
+  }
   int o = base + incl - c;
   for (int i = lo; i < hi; ++i) {
     if (masked[i]) {
@@ -463,7 +482,9 @@ template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 reduce_store_rope_kernel(const float* __restrict__ P, int rows, int ncols,
                          int rope_cols, const int32_t* __restrict__ pos,
-                         const float2* __restrict__ cs, T* __restrict__ out) {
+                         const float2* __restrict__ cs, T* __restrict__ out,
+                         int32_t* __restrict__ overflow) {
+  int nf = 0;
   const int row = blockIdx.x;
   const size_t stride = (size_t)rows * ncols;
   const float* pr = P + (size_t)row * ncols;
@@ -490,20 +511,22 @@ reduce_store_rope_kernel(const float* __restrict__ P, int rows, int ncols,
       a[i] = x[i] * cv[i] - y[i] * sv[i];
       b[i] = y[i] * cv[i] + x[i] * sv[i];
     }
-    store8<Fmt>(o + c1, a);
-    store8<Fmt>(o + c2, b);
+    nf += store8_count<Fmt>(o + c1, a);
+    nf += store8_count<Fmt>(o + c2, b);
   }
   for (int c = rope_cols + threadIdx.x * 8; c < ncols; c += kThreads * 8) {
     float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     sum_parts<KS>(pr + c, stride, x);
-    store8<Fmt>(o + c, x);
+    nf += store8_count<Fmt>(o + c, x);
   }
+  if (nf && overflow) atomicAdd(overflow, nf);
 }
 
 template <typename Fmt, int KS, typename T = typename Fmt::st>
 __global__ void __launch_bounds__(kThreads)
 reduce_swiglu_kernel(const float* __restrict__ P, int rows, int ffn,
-                     T* __restrict__ out) {
+                     T* __restrict__ out, int32_t* __restrict__ overflow) {
+  int nf = 0;
   const int row = blockIdx.x;
   const size_t ld = (size_t)2 * ffn;
   const size_t stride = (size_t)rows * ld;
@@ -515,8 +538,9 @@ reduce_swiglu_kernel(const float* __restrict__ P, int rows, int ffn,
     float h[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) h[i] = g[i] / (1.0f + __expf(-g[i])) * u[i];
-    store8<Fmt>(out + (size_t)row * ffn + c, h);
+    nf += store8_count<Fmt>(out + (size_t)row * ffn + c, h);
   }
+  if (nf && overflow) atomicAdd(overflow, nf);
 }
 
 // Element-type conversion through float32 (exact for the 16-bit sources),
@@ -627,26 +651,28 @@ int launch_reduce_add_gather(int dtype, const float* P, int ksplit, int rows,
 
 int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
                              int ncols, int rope_cols, const int32_t* pos,
-                             const float* cs, void* out, hipStream_t s) {
+                             const float* cs, void* out, hipStream_t s,
+                             int32_t* overflow) {
   if (rows <= 0) return DAVET_OK;
   if (rope_cols % 128 || ncols % 8)
     return set_error(DAVET_ESHAPE, "reduce_store_rope: column counts");
   ProfScope ps(KC_ROPE, s);
   DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
       (reduce_store_rope_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P,
-      rows, ncols, rope_cols, pos, (const float2*)cs, (F::st*)out)));
+      rows, ncols, rope_cols, pos, (const float2*)cs, (F::st*)out,
+      overflow)));
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }
 
 int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
-                         int ffn, void* out, hipStream_t s) {
+                         int ffn, void* out, hipStream_t s, int32_t* overflow) {
   if (rows <= 0) return DAVET_OK;
   if (ffn % 8) return set_error(DAVET_ESHAPE, "reduce_swiglu: ffn % 8 != 0");
   ProfScope ps(KC_MISC, s);
   DISPATCH16(dtype, DISPATCH_KS(ksplit, hipLaunchKernelGGL(
       (reduce_swiglu_kernel<F, KS>), dim3(rows), dim3(kThreads), 0, s, P, rows,
-      ffn, (F::st*)out)));
+      ffn, (F::st*)out, overflow)));
   DAVET_HIP(hipGetLastError());
   return DAVET_OK;
 }

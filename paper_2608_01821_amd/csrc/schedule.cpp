@@ -51,7 +51,7 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       const uint8_t* resp_masked, int32_t L, float* conf_out,
                       int32_t* argmax_out, float* logits_out, void* workspace,
                       size_t ws_bytes, const float* rope_cs, int rows_bound,
-                      hipStream_t stream);
+                      int clear_overflow, hipStream_t stream);
 
 // Host-side limit on one wait for a step's published levels (seconds).
 static std::atomic<double> g_wait_limit_s{120.0};
@@ -283,7 +283,7 @@ extern "C" int davet_run_schedule(
     int rc = denoise_step_impl(cfg, w, n_seqs, vptr.data(), nview.data(),
                                prompt_ids, cu_prompt, resp_ids, resp_masked, L,
                                conf, am, nullptr, workspace, ws_bytes, rope,
-                               rows_bound, stream);
+                               rows_bound, t == 1, stream);
     if (rc) return rc;
     rc = davet_unmask(n_seqs, L, k, conf, am, resp_ids, resp_masked, nullptr,
                       stream);

@@ -23,6 +23,7 @@
 namespace davet {
 
 struct Layout {
+  size_t flags;                        // 16-bit overflow counter (offset 0)
   size_t conf, argmax, argmax2;        // run_schedule scratch
   size_t X, A, QKV, O, H, rope, pos, list, slot, Hm, pmax, psum, parg, logits;
   size_t part;                         // split-K partial tiles (16-bit path)
@@ -54,6 +55,7 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
     p = align_up(p + bytes, 256);
     return at;
   };
+  o.flags = take(256);
   o.conf = take(rows * 4);
   o.argmax = take(rows * 4);
   o.argmax2 = take(rows * 4);    // the schedule loop's previous predictions
@@ -152,7 +154,7 @@ int denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                       const uint8_t* resp_masked, int32_t L, float* conf_out,
                       int32_t* argmax_out, float* logits_out, void* workspace,
                       size_t ws_bytes, const float* rope_cs, int rows_bound,
-                      hipStream_t stream);
+                      int clear_overflow, hipStream_t stream);
 }  // namespace davet
 
 extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
@@ -170,7 +172,21 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
                                   prompt_ids, cu_prompt, resp_ids, resp_masked,
                                   L, conf_out, argmax_out, logits_out,
                                   workspace, ws_bytes, nullptr, n_seqs * L,
-                                  stream);
+                                  1, stream);
+}
+
+extern "C" int davet_fp16_overflow_count(const void* workspace, int32_t* count,
+                                         hipStream_t stream) {
+  using namespace davet;
+  DAVET_CHECK_ARG(workspace && count, DAVET_EINVAL,
+                  "davet_fp16_overflow_count: null pointer");
+  DAVET_CHECK_ARG(((uintptr_t)workspace & 255) == 0, DAVET_EINVAL,
+                  "davet_fp16_overflow_count: workspace must be 256-byte aligned");
+  // the counter sits at offset 0 of every workspace layout
+  DAVET_HIP(hipMemcpyAsync(count, workspace, sizeof(int32_t),
+                         hipMemcpyDeviceToHost, stream));
+  DAVET_HIP(hipStreamSynchronize(stream));
+  return DAVET_OK;
 }
 
 // rope_cs: a rotary table already holding every position this step uses
@@ -178,6 +194,8 @@ extern "C" int davet_denoise_step(const davet_model_cfg* cfg,
 // rows_bound: an upper bound on the masked positions the caller knows on the
 // host (n_seqs * L when it knows none); it only sizes the head's grid, whose
 // workgroups still loop over any live rows beyond it.
+// clear_overflow: zero the workspace's overflow counter before this step's
+// stores (a schedule keeps counting over all its steps).
 int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                              int32_t n_seqs, const void* const* view_ptrs,
                              const int32_t* n_view, const int32_t* prompt_ids,
@@ -186,7 +204,8 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
                              float* conf_out, int32_t* argmax_out,
                              float* logits_out, void* workspace,
                              size_t ws_bytes, const float* rope_cs,
-                             int rows_bound, hipStream_t stream) {
+                             int rows_bound, int clear_overflow,
+                             hipStream_t stream) {
   using namespace davet;
   int rc = check_cfg(cfg);
   if (rc) return rc;
@@ -287,7 +306,9 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
     RUN(launch_rope_table(max_n, c.head_dim, c.rope_theta,
                           reinterpret_cast<float*>(ws + lay.rope), s));
   const float* g0 = c.n_layers > 0 ? w->layers[0].attn_norm : w->final_norm;
-  const RowList rl{n_seqs * L, list, conf_out, argmax_out, slot};
+  int32_t* overflow = reinterpret_cast<int32_t*>(ws + lay.flags);
+  const RowList rl{n_seqs * L, list,     conf_out,      argmax_out,
+                   slot,       overflow, clear_overflow};
   RUN(launch_assemble_norm(sp, vp, c.dtype, w->embed, prompt_ids, resp_ids,
                            resp_masked, c.mask_id, c.vocab, d, g0, c.rms_eps, X, A,
                            pos, rl, s));
@@ -305,10 +326,10 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
       // QKV projection, rotary embedding on the query and key columns
       RUN(launch_gemm16(dt, EPI_STORE, p_qkv, Ah, (const uint16_t*)lw.wqkv,
                         nullptr, QKV, T, 3 * d, d, 3 * d, pos, rope, 2 * d,
-                        part, part_cap, KC_GEMM_QKV, s));
+                        part, part_cap, KC_GEMM_QKV, s, overflow));
       if (p_qkv.ksplit > 1)
         RUN(launch_reduce_store_rope(dt, part, p_qkv.ksplit, T, 3 * d, 2 * d,
-                                     pos, rope, QKV, s));
+                                     pos, rope, QKV, s, overflow));
       RUN(launch_attention16(dt, (const uint16_t*)QKV, (uint16_t*)O, sp,
                              c.n_heads, c.head_dim, s));
       // X += O Wo^T, then A = RMSNorm(X) for the feed-forward block
@@ -322,9 +343,10 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
         RUN(launch_rmsnorm(X, T, d, lw.ffn_norm, c.rms_eps, c.dtype, A, s));
       RUN(launch_gemm16(dt, EPI_SWIGLU, p_gu, Ah, (const uint16_t*)lw.wg,
                         (const uint16_t*)lw.wu, H, T, 2 * F, d, F, nullptr,
-                        nullptr, 0, part, part_cap, KC_GEMM_GATEUP, s));
+                        nullptr, 0, part, part_cap, KC_GEMM_GATEUP, s,
+                        overflow));
       if (p_gu.ksplit > 1)
-        RUN(launch_reduce_swiglu(dt, part, p_gu.ksplit, T, F, H, s));
+        RUN(launch_reduce_swiglu(dt, part, p_gu.ksplit, T, F, H, s, overflow));
       // X += H Wd^T (and the next layer's input norm when reducing splits)
       RUN(launch_gemm16(dt, EPI_ADD_F32, p_dn, (const uint16_t*)H,
                         (const uint16_t*)lw.wd, nullptr, X, T, d, F, d,

@@ -131,6 +131,12 @@ def test_argument_validation_without_gpu():
                             C.c_void_p(16), C.c_void_p(16), None, None) == -1
     assert lib.davet_unmask(1, 2000, 2, C.c_void_p(16), C.c_void_p(16),
                             C.c_void_p(16), C.c_void_p(16), None, None) == -2
+    cnt = C.c_int32(7)
+    assert lib.davet_fp16_overflow_count(None, C.byref(cnt), None) == -1
+    assert lib.davet_fp16_overflow_count(C.c_void_p(256), None, None) == -1
+    assert lib.davet_fp16_overflow_count(C.c_void_p(16), C.byref(cnt),
+                                         None) == -1
+    assert cnt.value == 7
     cfg = dv.ModelCfg(1, 4096, 32, 128, 12288, 126464, 126463, 1e-5, 1e4,
                       dv.DAVET_BF16)
     assert dv.davet_workspace_bytes(cfg, 1000, 1, 128) > 0
