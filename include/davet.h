@@ -358,6 +358,21 @@ int davet_denoise_step(const davet_model_cfg* cfg, const davet_weights* w,
 int davet_fp16_overflow_count(const void* workspace, int32_t* count /*host*/,
                               hipStream_t stream);
 
+/* Key-range split of the 16-bit attention (process-wide setting).  A query
+ * tile's workgroup normally sweeps every key of its sequence (Sec. 3.1:
+ * bidirectional attention, every query sees every key).  When the ragged
+ * last query tiles of a launch would run as a thin extra round behind the
+ * full tiles, the library divides their keys among up to 8 workgroups, each
+ * writing fp32 partial softmax statistics and outputs into the workspace,
+ * and a merge kernel combines the pieces in a fixed order, so the result does
+ * not depend on timing; only the summation order differs from the unsplit
+ * launch.
+ *   mode 0: automatic (default); 1: never split; 2..8: split every query
+ *   tile into `mode` key ranges (a testing and tuning override; launches
+ *   whose partials would not fit in the workspace stay unsplit).
+ * Errors: EINVAL (mode outside [0, 8]). */
+int davet_set_attention_split(int32_t mode);
+
 /* --------------------------------------------------------------- unmask -- */
 
 /* Confidence-ranked commitment, Eq. (2) (Sec. 5.1: confidence ranking).  Per

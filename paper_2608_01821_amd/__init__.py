@@ -11,7 +11,7 @@ from ._lib import (  # noqa: F401
     LayerWeights, Mailbox, ModelCfg, Policy, ViewGeom, Weights, WeightsT,
     davet_set_wait_limit, default_mailbox,
     davet_build_views, davet_build_views_static, davet_convert, davet_demand_prior, davet_denoise_step,
-    davet_fp16_overflow_count,
+    davet_fp16_overflow_count, davet_set_attention_split,
     davet_head_tiled_elems, davet_pack_head, davet_parse_operation,
     davet_policy_envelope, davet_policy_step, davet_policy_step_device,
     davet_realizer_key_count,

@@ -105,6 +105,7 @@ _SIGS = {
                                      _vp, _i32, _vp, _vp, _vp, _vp, C.c_size_t,
                                      _vp]),
     "davet_fp16_overflow_count": (C.c_int, [_vp, _P_i32, _vp]),
+    "davet_set_attention_split": (C.c_int, [_i32]),
     "davet_unmask": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
                                _vp]),
     "davet_demand_prior": (C.c_double, [_i32]),
@@ -336,6 +337,11 @@ def davet_fp16_overflow_count(workspace, stream=None) -> int:
     _check(_L.davet_fp16_overflow_count(_ptr(workspace), C.byref(out),
                                         _stream(stream)))
     return out.value
+
+
+def davet_set_attention_split(mode):
+    """Attention key-range split: 0 automatic, 1 off, 2..8 forced."""
+    _check(_L.davet_set_attention_split(int(mode)))
 
 
 def davet_unmask(n_seqs, L, k, conf, argmax, resp_ids, resp_masked,

@@ -32,8 +32,18 @@
 // only when a score exceeds the current one by more than 2^8 in probability
 // (the probabilities, at most 2^8, stay well inside the 16-bit range and the
 // normaliser is an fp32 sum), so the O rescale is rare after the first tiles.
+//
+// Key-range split: when the query tiles alone would leave CUs idle (short
+// sequences), or leave a second round of workgroups for the ragged tiles,
+// a query tile's keys are divided among S workgroups ("pieces", contiguous
+// ranges of key tiles).  Each piece writes its (max, normaliser, unnormalised
+// O) in fp32 to a partial slot, and attn_merge_kernel combines the S pieces
+// in piece order (the result does not depend on which piece finishes first).
 
 #include "common.h"
+
+#include <algorithm>
+#include <atomic>
 
 namespace davet {
 namespace {
@@ -121,7 +131,8 @@ template <typename Fmt, int SPLIT>
 __global__ void __launch_bounds__(256 * SPLIT, (attn_minb<Fmt, SPLIT>()))
 attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
               SeqPack sp, int n_heads, int n_full, int n_ragged,
-              float scale_log2) {
+              float scale_log2, int s_full, int s_rag,
+              float* __restrict__ part) {
   using v8 = typename Fmt::v8;
   // SPLIT groups' double-buffered K/V tiles; after the loop the same bytes
   // hold the merge (O as [4 waves][4][16][64 lanes] floats, then max and
@@ -132,19 +143,29 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   constexpr int LDS_U16 = SPLIT * GROUP_LDS > MERGE_U16 ? SPLIT * GROUP_LDS
                                                         : MERGE_U16;
   __shared__ __attribute__((aligned(1024))) uint16_t smem[LDS_U16];
-  // blocks [0, n_heads * n_full): full tiles, head-major, XCD-remapped;
-  // then the ragged tiles, head-major
-  const int n_fb = n_heads * n_full;
-  int h, s, qt;
+  // blocks [0, n_heads * n_full * s_full): pieces of the full tiles,
+  // head-major, XCD-remapped; then the pieces of the ragged tiles,
+  // head-major.  Piece p of S takes key tiles [p*c, min(n_kt, (p+1)*c)),
+  // c = ceil(n_kt / S); with S > 1 it writes partial slot `slot`.
+  const int n_fb = n_heads * n_full * s_full;
+  int h, s, qt, piece, S, slot;
   if ((int)blockIdx.x < n_fb) {
     const int logical = remap_xcd_attn(blockIdx.x, n_fb);
-    h = logical / n_full;
-    locate_full(sp, logical % n_full, QT, s, qt);
+    const int tl = logical / s_full;
+    piece = logical % s_full;
+    S = s_full;
+    slot = logical;
+    h = tl / n_full;
+    locate_full(sp, tl % n_full, QT, s, qt);
   } else {
     const int r = blockIdx.x - n_fb;
     const int nr = max(n_ragged, 1);
-    h = r / nr;
-    locate_ragged(sp, r % nr, QT, s, qt);
+    const int tl = r / s_rag;
+    piece = r % s_rag;
+    S = s_rag;
+    slot = (s_full > 1 ? n_fb : 0) + r;
+    h = tl / nr;
+    locate_ragged(sp, tl % nr, QT, s, qt);
   }
   const int d = n_heads * HD;
   const size_t ld = (size_t)3 * d;
@@ -194,7 +215,10 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
     }
   };
   const int n_kt = (N + KT - 1) / KT;
-  const int n_it = (n_kt + SPLIT - 1) / SPLIT;     // same for every group
+  const int chunk = (n_kt + S - 1) / S;
+  const int kt0 = min(n_kt, piece * chunk);
+  const int kt1 = min(n_kt, kt0 + chunk);
+  const int n_it = (kt1 - kt0 + SPLIT - 1) / SPLIT;  // same for every group
 
   // the three parts of a key tile's work, on the K and V of one buffer
   auto qk_scores = [&](const char* Kb, f32x16 (&sc)[2]) {
@@ -296,8 +320,8 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
   if constexpr (BUFS == 1) {
     // one buffer, refilled once every wave is done with it (the other
     // workgroups on the CU hide the load)
-    if (n_kt > 0) issue(0, 0);
-    for (int kb = 0; kb < n_kt; ++kb) {
+    if (kt0 < kt1) issue(kt0, 0);
+    for (int kb = kt0; kb < kt1; ++kb) {
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
       sync_lds();
       if (live) {
@@ -309,18 +333,18 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       sync_lds();
-      if (kb + 1 < n_kt) issue(kb + 1, 0);
+      if (kb + 1 < kt1) issue(kb + 1, 0);
     }
   } else {
-    if (grp < n_kt) issue(grp, 0);
+    if (kt0 + grp < kt1) issue(kt0 + grp, 0);
     for (int it = 0; it < n_it; ++it) {
-      const int kb = it * SPLIT + grp;
-      const bool have = kb < n_kt && live;
+      const int kb = kt0 + it * SPLIT + grp;
+      const bool have = kb < kt1 && live;
       // this wave's loads of tile kb have landed, and its reads of the other
       // buffer are done; after the barrier, so are every wave's
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
       sync_lds();
-      if (kb + SPLIT < n_kt) issue(kb + SPLIT, (it + 1) & 1);
+      if (kb + SPLIT < kt1) issue(kb + SPLIT, (it + 1) & 1);
       if (have) {
         const char* Kb = gbuf + (it & 1) * (BUF_U16 * 2);
         f32x16 sc[2];
@@ -331,6 +355,16 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       }
     }
   }
+
+  // The lane's coordinates, derived again after the key loop so that they
+  // need not stay live in registers across it (the asm keeps the compiler
+  // from reusing the values computed before the loop).
+  int lane_e;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\t"
+               "v_mbcnt_hi_u32_b32 %0, -1, %0"
+               : "=v"(lane_e));
+  const int l32e = lane_e & 31, hhe = lane_e >> 5;
+  const int qe = qt * QT + wave * 32 + l32e;
 
   if constexpr (SPLIT == 2) {
     // group 1 hands (max, normaliser, O) of each query to group 0, once both
@@ -343,13 +377,13 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
       for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          mo[((wave * 4 + dt) * 16 + e) * 64 + lane] = o[dt][e];
-      ml[wave * 64 + lane] = m_run;
-      ml[256 + wave * 64 + lane] = l_run;
+          mo[((wave * 4 + dt) * 16 + e) * 64 + lane_e] = o[dt][e];
+      ml[wave * 64 + lane_e] = m_run;
+      ml[256 + wave * 64 + lane_e] = l_run;
     }
     __syncthreads();
     if (grp == 1) return;
-    const float m1 = ml[wave * 64 + lane], l1 = ml[256 + wave * 64 + lane];
+    const float m1 = ml[wave * 64 + lane_e], l1 = ml[256 + wave * 64 + lane_e];
     const float mm = fmaxf(m_run, m1);
     const float a0 = exp2f((m_run - mm) * scale_log2);
     const float a1 = exp2f((m1 - mm) * scale_log2);
@@ -358,17 +392,37 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
     for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
       for (int e = 0; e < 16; ++e)
-        o[dt][e] = o[dt][e] * a0 + mo[((wave * 4 + dt) * 16 + e) * 64 + lane] * a1;
+        o[dt][e] = o[dt][e] * a0 + mo[((wave * 4 + dt) * 16 + e) * 64 + lane_e] * a1;
   }
 
-  if (q < N) {
+  if (S > 1) {
+    // partial slot: O^T as [HD][QT] floats (lanes of a wave write 32
+    // consecutive queries of one dim), then max and normaliser as [2][QT]
+    if (qe < N) {
+      float* po = part + (size_t)slot * ATT_SLOT_FLOATS;
+      const int qr = wave * 32 + l32e;
+#pragma unroll
+      for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int dd = dt * 32 + (e >> 2) * 8 + hhe * 4 + (e & 3);
+          po[dd * QT + qr] = o[dt][e];
+        }
+      if (hhe == 0) {
+        po[HD * QT + qr] = m_run;
+        po[HD * QT + QT + qr] = l_run;
+      }
+    }
+    return;
+  }
+  if (qe < N) {
     const float inv = 1.0f / l_run;
-    uint16_t* op = out + (size_t)(row0 + q) * d + (size_t)h * HD;
+    uint16_t* op = out + (size_t)(row0 + qe) * d + (size_t)h * HD;
 #pragma unroll
     for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int dd = dt * 32 + g * 8 + hh * 4;
+        const int dd = dt * 32 + g * 8 + hhe * 4;
         u32x2 w;
         w[0] = (uint32_t)Fmt::store(o[dt][g * 4 + 0] * inv) |
                ((uint32_t)Fmt::store(o[dt][g * 4 + 1] * inv) << 16);
@@ -377,6 +431,76 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
         *reinterpret_cast<u32x2*>(op + dd) = w;
       }
   }
+}
+
+// Combines the S key-range pieces of each split query tile: with m the
+// largest piece maximum and w_p = 2^((m_p - m) * scale_log2), the output is
+// sum_p w_p O_p / sum_p w_p l_p, summed in piece order.  Eight workgroups per
+// split tile (tiles of the full class first when s_full > 1, then of the
+// ragged class); thread t of workgroup j takes query t % 128 and head dims
+// 16 j + 8 (t / 128) .. +8, and issues all of its loads at once (the merge
+// is latency-bound: a few MB over a few thousand threads).
+template <typename Fmt>
+__global__ void __launch_bounds__(256)
+attn_merge_kernel(const float* __restrict__ part, uint16_t* __restrict__ out,
+                  SeqPack sp, int n_heads, int n_full, int n_ragged,
+                  float scale_log2, int s_full, int s_rag) {
+  const int nfs = s_full > 1 ? n_heads * n_full : 0;
+  const int b = blockIdx.x >> 3;
+  int h, s, qt, S, slot0;
+  if (b < nfs) {
+    S = s_full;
+    slot0 = b * s_full;
+    h = b / n_full;
+    locate_full(sp, b % n_full, QT, s, qt);
+  } else {
+    const int tl = b - nfs;
+    const int nr = max(n_ragged, 1);
+    S = s_rag;
+    slot0 = (s_full > 1 ? n_heads * n_full * s_full : 0) + tl * s_rag;
+    h = tl / nr;
+    locate_ragged(sp, tl % nr, QT, s, qt);
+  }
+  const int row0 = sp.row0[s];
+  const int N = sp.row0[s + 1] - row0;
+  const int qr = threadIdx.x & (QT - 1);
+  const int d0 = ((blockIdx.x & 7) * 2 + (threadIdx.x >> 7)) * 8;
+  const int q = qt * QT + qr;
+  if (q >= N) return;
+  const float* base = part + (size_t)slot0 * ATT_SLOT_FLOATS;
+  float mv[ATT_MAX_SPLIT], lv[ATT_MAX_SPLIT], ov[ATT_MAX_SPLIT][8];
+#pragma unroll
+  for (int p = 0; p < ATT_MAX_SPLIT; ++p) {
+    if (p < S) {
+      const float* ps = base + (size_t)p * ATT_SLOT_FLOATS;
+      mv[p] = ps[HD * QT + qr];
+      lv[p] = ps[HD * QT + QT + qr];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ov[p][i] = ps[(d0 + i) * QT + qr];
+    }
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < ATT_MAX_SPLIT; ++p)
+    if (p < S) m = fmaxf(m, mv[p]);
+  float l = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < ATT_MAX_SPLIT; ++p) {
+    if (p < S) {
+      const float w = mv[p] == -INFINITY ? 0.f : exp2f((mv[p] - m) * scale_log2);
+      l += lv[p] * w;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] += ov[p][i] * w;
+    }
+  }
+  const float inv = 1.0f / l;
+  u32x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    v[i] = (uint32_t)Fmt::store(acc[2 * i] * inv) |
+           ((uint32_t)Fmt::store(acc[2 * i + 1] * inv) << 16);
+  *reinterpret_cast<u32x4*>(out + (size_t)(row0 + q) * (n_heads * HD) +
+                            (size_t)h * HD + d0) = v;
 }
 
 // fp32 path: one thread per (query, head), keys streamed with an online
@@ -419,9 +543,52 @@ attn_f32_kernel(const float* __restrict__ qkv, float* __restrict__ out,
 
 }  // namespace
 
+// 0: automatic; 1: never split; 2..ATT_MAX_SPLIT: split every query tile
+// that many ways (davet_set_attention_split)
+static std::atomic<int> g_attn_split_mode{0};
+
+size_t attention_part_bytes(int64_t tokens, int64_t seqs, int n_heads) {
+  const int64_t tiles = (tokens + QT - 1) / QT + seqs;
+  const int64_t slots =
+      std::min<int64_t>(ATT_MAX_SLOTS, tiles * n_heads * ATT_MAX_SPLIT);
+  return (size_t)slots * ATT_SLOT_FLOATS * sizeof(float);
+}
+
+// Key-range split factors (full tiles, ragged tiles) for a launch; depends
+// on the sequence layout only.  Automatic: a query tile's workgroup sweeps
+// every key, so when the ragged last tiles do not fit beside the last round
+// of full tiles they form a second round as long as a whole sweep; their
+// keys are then split (each piece at least four key tiles, 256 keys).
+// Short sequences are not split: there the per-workgroup latencies (query
+// load, first key tile, partial round trip) outweigh the idle CUs.
+static void plan_split(const SeqPack& sp, int n_heads, int n_full,
+                       int n_ragged, int slots, int& s_full, int& s_rag) {
+  s_full = s_rag = 1;
+  const int mode = g_attn_split_mode.load();
+  const int full_wg = n_heads * n_full, rag_wg = n_heads * n_ragged;
+  const int wg = full_wg + rag_wg;
+  if (wg == 0 || mode == 1) return;
+  if (mode >= 2) {
+    const int S = std::min(mode, ATT_MAX_SLOTS / wg);
+    if (S > 1) s_full = s_rag = S;
+    return;
+  }
+  int kt_rag_min = 1 << 30;
+  for (int i = 0; i < sp.n_seqs; ++i) {
+    const int n = sp.row0[i + 1] - sp.row0[i];
+    if (n % QT) kt_rag_min = std::min(kt_rag_min, (n + KT - 1) / KT);
+  }
+  if (rag_wg > 0 && wg > slots / 2 && rag_wg <= slots / 4 &&
+      rag_wg > (slots - full_wg % slots) % slots) {
+    int S = std::min({ATT_MAX_SPLIT, slots / rag_wg, kt_rag_min / 4});
+    S = std::min(S, ATT_MAX_SLOTS / rag_wg);
+    if (S > 1) s_rag = S;
+  }
+}
+
 int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
                        const SeqPack& sp, int n_heads, int head_dim,
-                       hipStream_t s) {
+                       float* part, size_t part_bytes, hipStream_t s) {
   if (head_dim != HD)
     return set_error(DAVET_ESHAPE, "attention16: head_dim must be 128");
   int n_full = 0, n_ragged = 0;
@@ -432,26 +599,56 @@ int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
   }
   const int tiles = n_full + n_ragged;
   if (tiles == 0) return DAVET_OK;
-  ProfScope ps(KC_ATTN, s);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
-  const dim3 grid(tiles * n_heads);
-  // Few workgroups (short sequences): two key groups per workgroup so each
-  // SIMD still holds two wavefronts.  Enough workgroups to fill the CUs: one
-  // key group each, three workgroups per CU (measured on MI355X against two
-  // groups: 3805 tokens 477 -> 443 us, 18020 tokens 8.45 -> 7.61 ms; 889
-  // tokens 36 vs 41 us the other way; one buffer at three workgroups per CU
-  // against two at two: 3805 tokens 325 -> 313 us, 18020 5.69 -> 5.42 ms).
-  const bool split = tiles * n_heads < 512;
+  // Workgroup slots of the one-key-group kernel: three per CU with fp16
+  // (single K/V buffer), two with bf16.
+  const int slots = (dtype == DAVET_F16 ? 3 : 2) * 256;
+  int s_full, s_rag;
+  plan_split(sp, n_heads, n_full, n_ragged, slots, s_full, s_rag);
+  const int split_slots = (s_full > 1 ? n_heads * n_full * s_full : 0) +
+                          (s_rag > 1 ? n_heads * n_ragged * s_rag : 0);
+  if (split_slots > 0 &&
+      (!part || (size_t)split_slots * ATT_SLOT_FLOATS * sizeof(float) > part_bytes))
+    s_full = s_rag = 1;                  // no room: the unsplit launch
+  const bool pieces = s_full > 1 || s_rag > 1;
+  const dim3 grid(n_heads * (n_full * s_full + n_ragged * s_rag));
+  // Few workgroups and no split (short sequences with few key tiles): two
+  // key groups per workgroup so each SIMD still holds two wavefronts.
+  // Otherwise one key group each, three workgroups per CU (measured on
+  // MI355X against two groups: 3805 tokens 477 -> 443 us, 18020 tokens 8.45
+  // -> 7.61 ms; 889 tokens 36 vs 41 us the other way; one buffer at three
+  // workgroups per CU against two at two: 3805 tokens 325 -> 313 us, 18020
+  // 5.69 -> 5.42 ms).
+  const bool two_groups = !pieces && tiles * n_heads < 512;
+  {
+    ProfScope ps(KC_ATTN, s);
 #define ATTN(F)                                                                \
-  if (split)                                                                   \
+  if (two_groups)                                                              \
     hipLaunchKernelGGL((attn16_kernel<F, 2>), grid, dim3(512), 0, s, qkv, o,   \
-                       sp, n_heads, n_full, n_ragged, scale_log2);             \
+                       sp, n_heads, n_full, n_ragged, scale_log2, s_full,      \
+                       s_rag, part);                                           \
   else                                                                         \
     hipLaunchKernelGGL((attn16_kernel<F, 1>), grid, dim3(256), 0, s, qkv, o,   \
-                       sp, n_heads, n_full, n_ragged, scale_log2)
-  if (dtype == DAVET_F16) { ATTN(F16); } else { ATTN(BF16); }
+                       sp, n_heads, n_full, n_ragged, scale_log2, s_full,      \
+                       s_rag, part)
+    if (dtype == DAVET_F16) { ATTN(F16); } else { ATTN(BF16); }
 #undef ATTN
-  DAVET_HIP(hipGetLastError());
+    DAVET_HIP(hipGetLastError());
+  }
+  if (pieces) {
+    ProfScope ps(KC_ATTN, s);
+    const int mgrid = 8 * ((s_full > 1 ? n_heads * n_full : 0) +
+                           (s_rag > 1 ? n_heads * n_ragged : 0));
+    if (dtype == DAVET_F16)
+      hipLaunchKernelGGL(attn_merge_kernel<F16>, dim3(mgrid), dim3(256), 0, s,
+                         part, o, sp, n_heads, n_full, n_ragged, scale_log2,
+                         s_full, s_rag);
+    else
+      hipLaunchKernelGGL(attn_merge_kernel<BF16>, dim3(mgrid), dim3(256), 0, s,
+                         part, o, sp, n_heads, n_full, n_ragged, scale_log2,
+                         s_full, s_rag);
+    DAVET_HIP(hipGetLastError());
+  }
   return DAVET_OK;
 }
 
@@ -474,3 +671,11 @@ int launch_attention_f32(const float* qkv, float* o, const SeqPack& sp,
 }
 
 }  // namespace davet
+
+extern "C" int davet_set_attention_split(int32_t mode) {
+  using namespace davet;
+  DAVET_CHECK_ARG(mode >= 0 && mode <= ATT_MAX_SPLIT, DAVET_EINVAL,
+                  "davet_set_attention_split: mode must be in [0, 8]");
+  g_attn_split_mode.store(mode);
+  return DAVET_OK;
+}

@@ -283,9 +283,18 @@ int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     const int32_t* m_count, hipStream_t s);
 
 // Attention over the packed batch: qkv [total, 3d] -> o [total, d]
+// Key-range split of the 16-bit attention: a query tile's keys may be
+// divided among up to ATT_MAX_SPLIT workgroups, each writing one partial slot
+// of ATT_SLOT_FLOATS floats (O^T as [128 dims][128 queries], then max and
+// normaliser as [2][128]) into `part`; at most ATT_MAX_SLOTS slots.
+constexpr int ATT_MAX_SPLIT = 8;
+constexpr int ATT_MAX_SLOTS = 1024;
+constexpr int ATT_SLOT_FLOATS = 128 * 128 + 2 * 128;
+// Partial bytes a launch over at most `tokens` rows in `seqs` sequences may use.
+size_t attention_part_bytes(int64_t tokens, int64_t seqs, int n_heads);
 int launch_attention16(int dtype, const uint16_t* qkv, uint16_t* o,
                        const SeqPack& sp, int n_heads, int head_dim,
-                       hipStream_t s);
+                       float* part, size_t part_bytes, hipStream_t s);
 int launch_convert(const void* src, int src_dtype, void* dst, int dst_dtype,
                    size_t n, hipStream_t s);
 int launch_attention_f32(const float* qkv, float* o, const SeqPack& sp,

@@ -77,7 +77,12 @@ static Layout make_layout(const davet_model_cfg& c, int64_t tokens,
   } else {
     o.logits = take((size_t)rows * c.vocab * 4);
   }
-  o.part = take(partial_bytes(c, tokens));
+  // split-K partials of the projections, and (not live at the same time)
+  // the key-range partials of attention
+  o.part = take(is16(c.dtype)
+                    ? std::max(partial_bytes(c, tokens),
+                               attention_part_bytes(tokens, seqs, c.n_heads))
+                    : 0);
   // Every region above grows with the token count, so a step with fewer
   // tokens than the workspace was sized for never reaches this one: the
   // schedule loop keeps its rotary table here for all its steps.
@@ -292,6 +297,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   int32_t* pos = reinterpret_cast<int32_t*>(ws + lay.pos);
   float* part = reinterpret_cast<float*>(ws + lay.part);
   const size_t part_cap = partial_bytes(c, total);
+  const size_t attn_part_cap = lay.rope_sched - lay.part;
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
   int32_t* slot = reinterpret_cast<int32_t*>(ws + lay.slot);
   void* Hm = ws + lay.Hm;
@@ -331,7 +337,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
         RUN(launch_reduce_store_rope(dt, part, p_qkv.ksplit, T, 3 * d, 2 * d,
                                      pos, rope, QKV, s, overflow));
       RUN(launch_attention16(dt, (const uint16_t*)QKV, (uint16_t*)O, sp,
-                             c.n_heads, c.head_dim, s));
+                             c.n_heads, c.head_dim, part, attn_part_cap, s));
       // X += O Wo^T, then A = RMSNorm(X) for the feed-forward block
       RUN(launch_gemm16(dt, EPI_ADD_F32, p_o, (const uint16_t*)O,
                         (const uint16_t*)lw.wo, nullptr, X, T, d, d, d,

@@ -105,6 +105,38 @@ def test_one_layer_full_size(one_layer, level, frac):
                   g_lg[0], 12, level)
 
 
+def test_attention_split_matches_unsplit(one_layer):
+    """The key-range split of attention at the 8B shape, against the same
+    call with the split off (davet_set_attention_split(1)): logits of the
+    masked rows within 1e-3 rel-RMS (only the fp32 summation order differs).
+    A four-crop sequence of 24 full query tiles and a ragged one per head
+    (3092 or 3188 tokens): automatically, the ragged tiles' keys split 8
+    ways behind one full round of 768 workgroups.  The workload's own coarse
+    view (356 or 1300 tokens) with every tile split 4 ways (forced)."""
+    cfg, mdl, sample = one_layer
+    c4 = synth.get_config(4)
+    s4 = synth.gen_sample(c4)
+    plen = 48 if cfg.resp_len == 128 else 16
+    four = Sample(cfg, 4, s4["visual"][0], s4["prompts"][0][:plen],
+                  oracle_values="model")
+    rng = np.random.default_rng(8)
+    ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.9)
+    rows = torch.from_numpy(np.nonzero(masked)[0]).cuda()
+    try:
+        for smp, level, split in ((four, 2, 0), (sample, 0, 4)):
+            dv.davet_set_attention_split(split)
+            a = gpu_step(cfg, mdl, [smp], [level], ids[None], masked[None])
+            dv.davet_set_attention_split(1)
+            b = gpu_step(cfg, mdl, [smp], [level], ids[None], masked[None])
+            err = rel_rms(a[2][0][rows].cpu().numpy(),
+                          b[2][0][rows].cpu().numpy())
+            say("  split %d vs unsplit, level %d: rel-RMS %.2e"
+                % (split, level, err))
+            assert err <= 1e-3
+    finally:
+        dv.davet_set_attention_split(0)
+
+
 def test_ragged16_full_size():
     """The 16-sequence ragged batch in one packed call; four sequences are
     checked against the oracle, each on its own.  Then the same call with the

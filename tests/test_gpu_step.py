@@ -11,8 +11,10 @@ import numpy as np
 import pytest
 import torch
 
+import paper_2608_01821_amd as dv
 import synth
 from gpu_util import (TOL, Model, Sample, compare, oracle_step, random_state,
+                      rel_rms,
                       run_gpu_step)
 
 pytestmark = pytest.mark.gpu
@@ -135,3 +137,43 @@ def test_step_edge_inputs():
                                       masked[i])
         compare(cfg, TOL[mdl.mode], masked[i], g_conf[i], g_am[i], g_lg[i],
                 pos, lg, am, cf)
+
+
+SPLIT_RTOL = {"f16": 1e-3, "bf16": 1e-2}
+
+
+@pytest.mark.parametrize("mode", ["f16", "bf16"])
+def test_key_split_attention(mode):
+    """Attention with every query tile's keys split among 2, 3 or 8
+    workgroups (davet_set_attention_split), merged by the merge kernel.  One
+    27x27 crop: 779 tokens at the full view (13 key tiles: pieces of 7, 5
+    and 2 tiles), 246 at the middle one (4 key tiles: with 8 pieces half of
+    them are empty).  Each run matches the oracle, and its logits stay close
+    to the unsplit launch's: only the fp32 summation order of the attention
+    differs, which moves the 16-bit rounding of some attention outputs by one
+    unit (fp16 2^-11, bf16 2^-8 relative), so rel-RMS within 1e-3 (fp16) or
+    1e-2 (bf16)."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_any_config(11), n_layers=1, grid=27,
+                              n_crops=1)
+    mdl = Model(cfg, mode)
+    s = synth.gen_sample(cfg)
+    sample = Sample(cfg, s["n_crops"][0], s["visual"][0], s["prompts"][0],
+                    mode)
+    rng = np.random.default_rng(31)
+    ids, masked = random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.8)
+    m = masked.astype(bool)
+    try:
+        for level in (2, 1):
+            pos, lg, am, cf = oracle_step(cfg, mdl, sample, level, ids, masked)
+            dv.davet_set_attention_split(1)
+            _, _, u_lg = run_gpu_step(cfg, mdl, [sample], [level], ids, masked)
+            for split in (2, 3, 8):
+                dv.davet_set_attention_split(split)
+                g_conf, g_am, g_lg = run_gpu_step(cfg, mdl, [sample], [level],
+                                                  ids, masked)
+                compare(cfg, TOL[mode], masked, g_conf[0], g_am[0], g_lg[0],
+                        pos, lg, am, cf)
+                assert rel_rms(g_lg[0][m], u_lg[0][m]) <= SPLIT_RTOL[mode]
+    finally:
+        dv.davet_set_attention_split(0)

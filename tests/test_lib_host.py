@@ -137,6 +137,9 @@ def test_argument_validation_without_gpu():
     assert lib.davet_fp16_overflow_count(C.c_void_p(16), C.byref(cnt),
                                          None) == -1
     assert cnt.value == 7
+    assert lib.davet_set_attention_split(-1) == -1
+    assert lib.davet_set_attention_split(9) == -1
+    assert lib.davet_set_attention_split(0) == 0
     cfg = dv.ModelCfg(1, 4096, 32, 128, 12288, 126464, 126463, 1e-5, 1e4,
                       dv.DAVET_BF16)
     assert dv.davet_workspace_bytes(cfg, 1000, 1, 128) > 0
