@@ -92,7 +92,32 @@ def parse():
                     help="only stream MIB MiB of fp32 through a plain "
                          "elementwise copy (y = x * 1) five times and exit: "
                          "the known-size reference for HBM byte counters")
+    ap.add_argument("--views-probe", action="store_true",
+                    help="only build the pooled evidence views of one, four "
+                         "and five 27x27 crops (d = 4096, fp16, K = 3) 20 "
+                         "times each and exit: the launches the view-build "
+                         "profile summarises")
     return ap.parse_args()
+
+
+def views_probe():
+    """davet_build_views at the 8B shape: one, four and five 27x27 crops of
+    seeded random fp16 encodings, 20 launches per geometry."""
+    import torch
+    import paper_2608_01821_amd as dv
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    for crops in (1, 4, 5):
+        g = dv.ViewGeom(crops, 27, 4096, 3, dv.DAVET_F16, 0, 0)
+        sizes = dv.davet_view_sizes(g)
+        v = torch.randn(crops * 729, 4096, device="cuda",
+                        generator=gen).half().view(torch.int16)
+        levels = [torch.empty((sizes[l], 4096), dtype=torch.int16,
+                              device="cuda") for l in range(2)]
+        for _ in range(20):
+            dv.davet_build_views(g, v, levels)
+        torch.cuda.synchronize()
+        print(json.dumps({"views_probe_crops": crops, "sizes": sizes,
+                          "launches": 20}), flush=True)
 
 
 def copy_calibration(mib):
@@ -500,6 +525,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.views_probe:
+        views_probe()
         return
     import torch
     import synth
