@@ -297,6 +297,7 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   int32_t* pos = reinterpret_cast<int32_t*>(ws + lay.pos);
   float* part = reinterpret_cast<float*>(ws + lay.part);
   const size_t part_cap = partial_bytes(c, total);
+  // the partial region ends where the schedule's rotary table begins
   const size_t attn_part_cap = lay.rope_sched - lay.part;
   int32_t* list = reinterpret_cast<int32_t*>(ws + lay.list);
   int32_t* slot = reinterpret_cast<int32_t*>(ws + lay.slot);
