@@ -54,11 +54,25 @@ def test_step_deterministic(small):
         assert np.array_equal(x, y, equal_nan=True)
 
 
-@pytest.mark.parametrize("cid,mode", [(12, "f16"), (12, "bf16"), (13, "f32")])
-def test_ragged_batch_step(cid, mode):
+@pytest.mark.parametrize("cid,mode,split", [(12, "f16", 0), (12, "bf16", 0),
+                                            (13, "f32", 0), (12, "f16", 3),
+                                            (12, "bf16", 8)])
+def test_ragged_batch_step(cid, mode, split):
     """Packed batch of sequences with different view levels and prompt
     lengths in one call; each sequence must equal its own oracle run (the
-    attention of one sequence never sees another's tokens)."""
+    attention of one sequence never sees another's tokens).  Also with the
+    keys of every query tile split 3 or 8 ways (forced), so that pieces and
+    their merge map onto the right sequence and tile across a ragged batch,
+    including empty pieces of short sequences."""
+    if split:
+        dv.davet_set_attention_split(split)
+    try:
+        _ragged_batch_step(cid, mode)
+    finally:
+        dv.davet_set_attention_split(0)
+
+
+def _ragged_batch_step(cid, mode):
     cfg = synth.get_any_config(cid)
     mdl = Model(cfg, mode)
     s = synth.gen_sample(cfg)
@@ -96,11 +110,22 @@ def test_step_without_layers(cid, mode):
             am, cf)
 
 
-def test_step_edge_inputs():
+@pytest.mark.parametrize("split", [0, 4])
+def test_step_edge_inputs(split):
     """Edge inputs in one packed call: a sequence with neither view tokens
     nor prompt (only its response), one with a view but no prompt, one with
     every position already committed (conf -inf, argmax -1, logit rows
-    untouched), next to an ordinary one; each against its own oracle run."""
+    untouched), next to an ordinary one; each against its own oracle run.
+    Also with attention's keys split 4 ways (forced)."""
+    if split:
+        dv.davet_set_attention_split(split)
+    try:
+        _step_edge_inputs()
+    finally:
+        dv.davet_set_attention_split(0)
+
+
+def _step_edge_inputs():
     import copy
     cfg = synth.get_any_config(12)
     mdl = Model(cfg)
