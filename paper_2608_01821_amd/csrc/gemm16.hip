@@ -186,6 +186,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, hh = lane >> 5;
+  const int l16 = lane & 15, k4 = lane >> 4;
   const bool dual = (EPI == EPI_SWIGLU) || (EPI == EPI_PARTIAL && ep.dual);
 
   // ---- per-lane sources of this wave's load instructions (fixed over K)
@@ -247,13 +248,17 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       dma16(b_src[q] + boff, sb + (wave * BI + q) * 1024);
   };
 
-  f32x16 acc[TM][TN];
+  // acc[i][j][q]: the 16 x 16 block (q >> 1, q & 1) of the wave's 32 x 32
+  // block (i, j), one v_mfma_f32_16x16x32 accumulator each
+  f32x4 acc[TM][TN][4];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][q][e] = 0.f;
 
   // 32-row sub-tiles of this wave holding live rows: always a prefix, NL of
   // them.  The K loop is instantiated per NL, so its body has no branch
@@ -276,31 +281,35 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       if constexpr (NL > 0) {
         const char* sa = smem + (it % STAGES) * S_BYTES;
         const char* sb = sa + A_BYTES;
-        // fragments of K step kk+1 are read from LDS while the matrix ops of
-        // step kk run (two register sets)
-        v8 af[2][NL], bfr[2][TN];
-        auto load_frags = [&](int kk, v8 (&a)[NL], v8 (&b)[TN]) {
-          const int c = kk * 2 + hh;
+        // 32-deep K steps of 16 x 16 x 32 matrix ops: lane l supplies row
+        // (or column) l % 16 of a 16-row fragment and k = 8 (l / 16) .. +7,
+        // i.e. 16-byte chunk 4 kk + l / 16 of that LDS row
 #pragma unroll
-          for (int i = 0; i < NL; ++i) {
-            const int r = wm * WROWS + i * 32 + l32;
-            a[i] = *reinterpret_cast<const v8*>(sa + swz<BK>(r, c));
-          }
+        for (int kk = 0; kk < BK / 32; ++kk) {
+          const int c = kk * 4 + k4;
+          v8 af[NL][2], bfr[TN][2];
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int r = j * 64 + wn * 32 + l32;
-            b[j] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
-          }
-        };
-        load_frags(0, af[0], bfr[0]);
+          for (int i = 0; i < NL; ++i)
 #pragma unroll
-        for (int kk = 0; kk < BK / 16; ++kk) {
-          if (kk + 1 < BK / 16) load_frags(kk + 1, af[(kk + 1) & 1], bfr[(kk + 1) & 1]);
+            for (int h = 0; h < 2; ++h) {
+              const int r = wm * WROWS + i * 32 + h * 16 + l16;
+              af[i][h] = *reinterpret_cast<const v8*>(sa + swz<BK>(r, c));
+            }
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int r = j * 64 + wn * 32 + h * 16 + l16;
+              bfr[j][h] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
+            }
 #pragma unroll
           for (int i = 0; i < NL; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-              acc[i][j] = Fmt::mfma32(af[kk & 1][i], bfr[kk & 1][j], acc[i][j]);
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                acc[i][j][q] = Fmt::mfma16(af[i][q >> 1], bfr[j][q & 1],
+                                           acc[i][j][q]);
         }
       }
     }
@@ -315,91 +324,103 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   }
 
   // ---------------------------------------------------------------- epilogue
-  // acc[i][j][e]: row = wm*WROWS + i*32 + (e/4)*8 + (lane/32)*4 + e%4,
-  //               col = j*64 + wn*32 + lane%32   (tile-local)
-  const int hrow = hh * 4;
+  // acc[i][j][q][u]: row = wm*WROWS + i*32 + (q>>1)*16 + (lane/16)*4 + t,
+  //                  col = j*64 + wn*32 + (q&1)*16 + lane%16   (tile-local)
+  // so a lane's column in each 64-column group j is wn*32 + (q&1)*16 + l16
   int nf = 0;     // non-finite 16-bit values stored by this lane
+  const int rrow = k4 * 4;
   if constexpr (EPI == EPI_STORE) {
     uint16_t* C = reinterpret_cast<uint16_t*>(ep.C);
     const bool rope = ep.pos && n0 < ep.rope_cols;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
-        if (row >= M) continue;
-        uint16_t* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + l32;
-        if (rope) {
-          // j even / j+1: dims i and i+64 of the head starting at n0 + j*64
-          const float2 c = ep.cs[(size_t)ep.pos[row] * 64 + wn * 32 + l32];
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-          for (int j = 0; j < TN; j += 2) {
-            const float x = acc[i][j][e], y = acc[i][j + 1][e];
-            const uint16_t a = Fmt::store(x * c.x - y * c.y);
-            const uint16_t b = Fmt::store(y * c.x + x * c.y);
-            nf += Fmt::nonfinite(a) + Fmt::nonfinite(b);
-            crow[j * 64] = a;
-            crow[(j + 1) * 64] = b;
-          }
-        } else {
+        for (int u = 0; u < 4; ++u) {
+          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          if (row >= M) continue;
+          const int cl = wn * 32 + (q & 1) * 16 + l16;
+          uint16_t* crow = C + (size_t)row * ep.ldc + n0 + cl;
+          if (rope) {
+            // j even / j+1: dims cl and cl+64 of the head starting at n0 + j*64
+            const float2 c = ep.cs[(size_t)ep.pos[row] * 64 + cl];
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const uint16_t a = Fmt::store(acc[i][j][e]);
-            nf += Fmt::nonfinite(a);
-            crow[j * 64] = a;
+            for (int j = 0; j < TN; j += 2) {
+              const float x = acc[i][j][q][u], y = acc[i][j + 1][q][u];
+              const uint16_t a = Fmt::store(x * c.x - y * c.y);
+              const uint16_t b = Fmt::store(y * c.x + x * c.y);
+              nf += Fmt::nonfinite(a) + Fmt::nonfinite(b);
+              crow[j * 64] = a;
+              crow[(j + 1) * 64] = b;
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              const uint16_t a = Fmt::store(acc[i][j][q][u]);
+              nf += Fmt::nonfinite(a);
+              crow[j * 64] = a;
+            }
           }
         }
-      }
   } else if constexpr (EPI == EPI_ADD_F32) {
     float* C = reinterpret_cast<float*>(ep.C);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
-        if (row >= M) continue;
-        float* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + l32;
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) crow[j * 64] += acc[i][j][e];
-      }
+        for (int u = 0; u < 4; ++u) {
+          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          if (row >= M) continue;
+          float* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + (q & 1) * 16 + l16;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) crow[j * 64] += acc[i][j][q][u];
+        }
   } else if constexpr (EPI == EPI_SWIGLU) {
     uint16_t* C = reinterpret_cast<uint16_t*>(ep.C);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
-        if (row >= M) continue;
-        uint16_t* crow = C + (size_t)row * ep.ldc + nb * (BN / 2) + wn * 32 + l32;
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int j = 0; j < TN / 2; ++j) {
-          const float g = acc[i][j][e], u = acc[i][j + TN / 2][e];
-          const uint16_t h = Fmt::store(g / (1.0f + __expf(-g)) * u);
-          nf += Fmt::nonfinite(h);
-          crow[j * 64] = h;
+        for (int u = 0; u < 4; ++u) {
+          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          if (row >= M) continue;
+          uint16_t* crow = C + (size_t)row * ep.ldc + nb * (BN / 2) + wn * 32 +
+                           (q & 1) * 16 + l16;
+#pragma unroll
+          for (int j = 0; j < TN / 2; ++j) {
+            const float g = acc[i][j][q][u], up = acc[i][j + TN / 2][q][u];
+            const uint16_t h = Fmt::store(g / (1.0f + __expf(-g)) * up);
+            nf += Fmt::nonfinite(h);
+            crow[j * 64] = h;
+          }
         }
-      }
   } else if constexpr (EPI == EPI_PARTIAL) {
     float* P = ep.part + (size_t)ks * M * ep.part_ld;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
-        if (row >= M) continue;
-        float* prow = P + (size_t)row * ep.part_ld;
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          int col;
-          if (ep.dual) {       // gate half -> [0, F), up half -> [F, 2F)
-            const int jj = j % (TN / 2);
-            col = (j < TN / 2 ? 0 : ep.ffn) + nb * (BN / 2) + jj * 64 + wn * 32 + l32;
-          } else {
-            col = n0 + j * 64 + wn * 32 + l32;
+        for (int u = 0; u < 4; ++u) {
+          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          if (row >= M) continue;
+          float* prow = P + (size_t)row * ep.part_ld;
+          const int cl = wn * 32 + (q & 1) * 16 + l16;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            int col;
+            if (ep.dual) {       // gate half -> [0, F), up half -> [F, 2F)
+              const int jj = j % (TN / 2);
+              col = (j < TN / 2 ? 0 : ep.ffn) + nb * (BN / 2) + jj * 64 + cl;
+            } else {
+              col = n0 + j * 64 + cl;
+            }
+            prow[col] = acc[i][j][q][u];
           }
-          prow[col] = acc[i][j][e];
         }
-      }
   } else {   // EPI_HEAD
     __shared__ float red_m[2][BM];
     __shared__ float red_s[2][BM];
@@ -407,41 +428,50 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int lrow = wm * WROWS + i * 32 + (e >> 2) * 8 + hrow + (e & 3);
-        const int row = m0 + lrow;
-        float m = -INFINITY, s = 0.f;
-        int a = 0x7fffffff;
+      for (int qr = 0; qr < 2; ++qr) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = n0 + j * 64 + wn * 32 + l32;
-          float v = acc[i][j][e];
-          if (ep.logits_out && row < m_live && col < ep.vocab)
-            ep.logits_out[(size_t)ep.list[1 + row] * ep.vocab + col] = v;
-          if (col == ep.mask_id || col >= ep.vocab) v = -INFINITY;
-          if (v > m) {              // columns ascend with j: keeps the first
-            s = s * __expf(m - v) + 1.0f;
-            m = v; a = col;
-          } else if (v != -INFINITY) {
-            s += __expf(v - m);
+        for (int u = 0; u < 4; ++u) {
+          const int lrow = wm * WROWS + i * 32 + qr * 16 + rrow + u;
+          const int row = m0 + lrow;
+          float m = -INFINITY, s = 0.f;
+          int a = 0x7fffffff;
+          // this lane's columns of the row, ascending: j*64 + wn*32 +
+          // qc*16 + l16 for j, then qc
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+#pragma unroll
+            for (int qc = 0; qc < 2; ++qc) {
+              const int col = n0 + j * 64 + wn * 32 + qc * 16 + l16;
+              float v = acc[i][j][qr * 2 + qc][u];
+              if (ep.logits_out && row < m_live && col < ep.vocab)
+                ep.logits_out[(size_t)ep.list[1 + row] * ep.vocab + col] = v;
+              if (col == ep.mask_id || col >= ep.vocab) v = -INFINITY;
+              if (v > m) {              // columns ascend: keeps the first
+                s = s * __expf(m - v) + 1.0f;
+                m = v; a = col;
+              } else if (v != -INFINITY) {
+                s += __expf(v - m);
+              }
+            }
           }
-        }
+          // the 16 lanes holding this row (same lane / 16)
 #pragma unroll
-        for (int o = 1; o < 32; o <<= 1) {
-          const float m2 = __shfl_xor(m, o, 64);
-          const float s2 = __shfl_xor(s, o, 64);
-          const int a2 = __shfl_xor(a, o, 64);
-          const float mm = fmaxf(m, m2);
-          float ns = 0.f;
-          if (m != -INFINITY) ns += s * __expf(m - mm);
-          if (m2 != -INFINITY) ns += s2 * __expf(m2 - mm);
-          const int na = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
-          m = mm; s = ns; a = na;
-        }
-        if (l32 == 0) {
-          red_m[wn][lrow] = m;
-          red_s[wn][lrow] = s;
-          red_a[wn][lrow] = a;
+          for (int o = 1; o < 16; o <<= 1) {
+            const float m2 = __shfl_xor(m, o, 64);
+            const float s2 = __shfl_xor(s, o, 64);
+            const int a2 = __shfl_xor(a, o, 64);
+            const float mm = fmaxf(m, m2);
+            float ns = 0.f;
+            if (m != -INFINITY) ns += s * __expf(m - mm);
+            if (m2 != -INFINITY) ns += s2 * __expf(m2 - mm);
+            const int na = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
+            m = mm; s = ns; a = na;
+          }
+          if (l16 == 0) {
+            red_m[wn][lrow] = m;
+            red_s[wn][lrow] = s;
+            red_a[wn][lrow] = a;
+          }
         }
       }
     }
