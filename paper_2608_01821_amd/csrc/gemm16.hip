@@ -1,16 +1,20 @@
 // 16-bit (fp16 or bf16) matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] B[N,K]^T
 // with both operands K-contiguous (activations row-major, weights [out, in]).
 //
-// CDNA4 design.  A 256-thread workgroup (2 x 2 wavefronts) owns a BM x BN
-// tile; each wavefront issues v_mfma_f32_32x32x16 on (BM/2) x (BN/2).  K moves
-// in slabs of 32 through a 4-deep ring of LDS stages filled by direct
-// global->LDS loads (global_load_lds_dwordx4: no VGPR staging), so up to three
-// slabs are in flight while one feeds the matrix cores; one barrier per slab.
-// Each LDS row is 64 bytes (4 chunks of 16 B); chunk c of row r sits in slot
-// c ^ ((r >> 2) & 3), which spreads the 16-byte fragment reads of 16
-// consecutive rows over distinct bank groups.  Workgroup ids are remapped so
-// each XCD (ids congruent mod 8) walks a contiguous run of tiles, M fastest:
-// a weight tile is fetched into one XCD's L2 and reused by every M tile.
+// CDNA4 design.  A workgroup of 4, 8 or 16 wavefronts (a WM x 2 grid) owns a
+// BM x BN tile; each wavefront accumulates (BM/WM) x (BN/2) with
+// v_mfma_f32_16x16x32 ops (fp32 accumulators).  K moves in slabs of BK (32
+// or 64) through a STAGES-deep ring of LDS stages filled by direct
+// global->LDS loads (global_load_lds_dwordx4: no VGPR staging), so up to
+// STAGES - 1 slabs are in flight while one feeds the matrix cores; one
+// barrier per slab.  Each LDS row holds BK 16-bit values in 16-byte chunks;
+// chunk c of row r sits in slot c ^ ((r / rows-per-256-bytes) % chunks),
+// which spreads the 16-byte fragment reads of 16 consecutive rows over
+// distinct bank groups.  Workgroup ids are remapped so each XCD (ids
+// congruent mod 8) walks a contiguous run of tiles, M fastest: a weight tile
+// is fetched into one XCD's L2 and reused by every M tile.  The variants
+// (tile, slab depth, ring depth, waves) and the plan that picks one per
+// product shape are listed after the kernel.
 //
 // Split-K: with few output tiles (short sequences) the K range is cut into
 // ksplit parts whose fp32 partial tiles land in a workspace; a row kernel
@@ -601,7 +605,10 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 // another plan beat by more than 5 % in both of two repetitions (a fourth,
 // QKV at 209 rows with 5 splits, measured 1.2 % slower inside the step: its
 // larger partials cost the reduction more than the sweep's cold-cache timing
-// shows, and was left out).
+// shows, and was left out).  After the move to 16 x 16 x 32 matrix ops a
+// third sweep (variants 4, 6-9 and 12-14, splits 1-6 and 8, the split-K
+// reduction or the following norm included) changed thirteen entries whose
+// new plan was more than 4 % faster in each of three repetitions.
 // Because the number of row tiles and of waves of workgroups changes in
 // steps, the best plan is jagged in M; a product of M rows takes the plan of
 // the nearest sample point in log M.
@@ -613,13 +620,13 @@ constexpr int kNP = 26;
 struct TableShape { int N, K; GemmPlan plan[kNP]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4, 0}, {14, 2, 0}, {13, 2, 0}, {13, 2, 0}, {13, 2, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 2, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {12288, 4096, {{8, 4, 0}, {14, 2, 0}, {13, 2, 0}, {13, 2, 0}, {13, 2, 0}, {12, 1, 0}, {14, 2, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {14, 2, 0}, {14, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8, 0}, {6, 5, 0}, {6, 4, 0}, {6, 4, 0}, {12, 4, 0}, {6, 3, 0}, {14, 4, 0}, {14, 4, 0}, {6, 2, 0}, {6, 2, 0}, {8, 3, 0}, {14, 2, 0}, {14, 2, 0}, {12, 1, 0}, {12, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {4096, 4096, {{6, 8, 0}, {6, 5, 0}, {6, 4, 0}, {6, 4, 0}, {12, 4, 0}, {6, 3, 0}, {14, 4, 0}, {12, 2, 0}, {6, 2, 0}, {6, 2, 0}, {8, 3, 0}, {14, 2, 0}, {14, 2, 0}, {12, 1, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // gate + up: N = 2 ffn, K = d
     {24576, 4096, {{8, 2, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{12, 8, 0}, {14, 8, 0}, {14, 8, 0}, {8, 8, 0}, {8, 8, 0}, {12, 3, 0}, {14, 4, 0}, {14, 4, 0}, {8, 4, 0}, {8, 4, 0}, {13, 3, 0}, {14, 2, 0}, {14, 2, 0}, {8, 2, 0}, {8, 2, 0}, {8, 3, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {4096, 12288, {{12, 8, 0}, {14, 8, 0}, {14, 8, 0}, {8, 8, 0}, {8, 8, 0}, {6, 3, 0}, {13, 5, 0}, {14, 4, 0}, {13, 4, 0}, {8, 4, 0}, {13, 3, 0}, {14, 2, 0}, {14, 2, 0}, {13, 2, 0}, {8, 2, 0}, {8, 3, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 2, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
 };
 
 // Point i serves the rows up to the geometric mean of points i and i+1.
