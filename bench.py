@@ -364,10 +364,12 @@ def kernel_rooflines(cfg, kern, work):
     return out
 
 
-def per_level_steps(cfg, st, levels, reps=10):
+def per_level_steps(cfg, st, levels, reps=10, profile=True):
     """Denoising step time at every view level (the loop's own kernels, one
     davet_denoise_step + davet_unmask on every sequence at that level, all
-    response positions masked), timed with events; untimed by the bench."""
+    response positions masked), timed with events; untimed by the bench.
+    With `profile`, one further step per level carries events around every
+    launch and gives each matrix kernel class's rate at that level."""
     import torch
     dv = st["dv"]
     n, L, K = cfg.n_seqs, cfg.resp_len, cfg.K
@@ -397,9 +399,38 @@ def per_level_steps(cfg, st, levels, reps=10):
                 times.append(e0.elapsed_time(e1))
         times.sort()
         ms = times[len(times) // 2]
-        out[str(lv)] = dict(tokens=sum(nview) + st["cu"][-1] + n * L,
-                            ms_per_step=round(ms, 4),
+        tokens = sum(nview) + st["cu"][-1] + n * L
+        out[str(lv)] = dict(tokens=tokens, ms_per_step=round(ms, 4),
                             steps_per_s=round(1e3 / ms, 2))
+        if profile and cfg.dtype == "bf16":
+            # one more step with events around every launch: each matrix
+            # class's rate at this level against the 2.5 PF peak
+            st["ids"].fill_(cfg.mask_id)
+            st["msk"].fill_(1)
+            torch.cuda.synchronize()
+            dv.prof_enable(12 * cfg.n_layers + 64)
+            dv.davet_denoise_step(st["mcfg"], st["W"], views, nview,
+                                  st["prompt"], st["cu"], st["ids"], st["msk"],
+                                  L, conf, am, None, st["ws"])
+            torch.cuda.synchronize()
+            kern = dv.prof_read()
+            dv.prof_enable(0)
+            d, F = cfg.d, cfg.ffn
+            lens = [nview[i] + st["cu"][i + 1] - st["cu"][i] + L
+                    for i in range(n)]
+            flops = {"gemm_qkv": 2.0 * tokens * d * 3 * d,
+                     "gemm_o": 2.0 * tokens * d * d,
+                     "gemm_gateup": 2.0 * tokens * d * 2 * F,
+                     "gemm_down": 2.0 * tokens * F * d,
+                     "attention": sum(4.0 * m * m * d for m in lens)}
+            rates = {}
+            for name, fl in flops.items():
+                cnt, kms = kern.get(name, (0, 0.0))
+                if cnt and kms > 0:
+                    ach = cfg.n_layers * fl / (kms / 1e3) / 1e12
+                    rates[name] = dict(achieved=round(ach, 1),
+                                       frac=round(ach / PEAK_BF16_TFLOPS, 4))
+            out[str(lv)]["matrix_rooflines_one_step"] = rates
     return out
 
 
@@ -609,7 +640,8 @@ def main():
                         us_per_step=round((ms_loop - fixed_ms) / cfg.steps
                                           * 1e3, 2),
                         share=round((ms_loop - fixed_ms) / ms_loop, 5))
-    levels_probe = per_level_steps(cfg, st, levels)
+    levels_probe = per_level_steps(cfg, st, levels,
+                                   profile=not args.no_kernel_timing)
     cpu = None
     if not args.no_cpu_baseline:
         try:
