@@ -236,7 +236,6 @@ enum Epilogue { EPI_STORE = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
 struct GemmPlan {
   int tile;      // kernel variant (tile shape, K slab, stages, waves)
   int ksplit;    // > 1: fp32 partials [ksplit][M][N] + a reduction kernel
-  int krot;      // > 0: N tile nb starts its K loop at slab nb*krot (mod)
 };
 // Tile shape and K split for an M x N x K product (N = 2*ffn for SwiGLU).
 GemmPlan plan_gemm16(int M, int N, int K);
@@ -274,16 +273,17 @@ int launch_reduce_store_rope(int dtype, const float* P, int ksplit, int rows,
 int launch_reduce_swiglu(int dtype, const float* P, int ksplit, int rows,
                          int ffn, void* out, hipStream_t s,
                          int32_t* overflow = nullptr);
+// Vocabulary head over the masked rows: the tile follows the weight layout
+// (tiled: davet_pack_head blocks) and live_bound, a host-side bound on the
+// live rows (-1: max_rows)
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s, int variant = -1,
-                  int krot = -1, int tiled = 0, int live_bound = -1);
-// vocabulary slabs per row (pmax/psum/parg columns) the head launch with
-// this variant (-1: the default for the layout and the live-row bound)
-// writes; at most ceil(V / 128)
-int head16_slabs(int vocab, int variant = -1, int tiled = 0,
-                 int live_bound = 1);
+                  float* logits_out, hipStream_t s, int tiled = 0,
+                  int live_bound = -1);
+// vocabulary slabs per row (pmax/psum/parg columns) the head launch for this
+// layout and live-row bound writes; at most ceil(V / 128)
+int head16_slabs(int vocab, int tiled = 0, int live_bound = 1);
 int launch_gemm_f32(int epi, const float* A, const float* B, const float* B2,
                     float* C, int M, int N, int K, int ldc, int cls,
                     const int32_t* m_count, hipStream_t s);

@@ -41,14 +41,10 @@ namespace {
 
 constexpr int BK_MIN = 32;   // K must be a multiple of this
 
-// K-order rotation of the vocabulary head (see launch_head16)
-#ifndef DAVET_HEAD_KROT
-#define DAVET_HEAD_KROT 0
-#endif
 constexpr int EPI_HEAD = 3;
 
 // Kernel variants: tile BM x BN, K slab BK (64-byte or 128-byte LDS rows),
-// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2 grid).
+// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2, 16: 8x2).
 template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_>
 struct Var {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_,
@@ -78,14 +74,9 @@ struct EpiArgs {
   int part_ld;
   int dual;              // B/B2 gate/up weights (SwiGLU), also for partials
   int ffn;
-  // K order: N tile nb starts at slab (nb * krot) mod nk and wraps, so that
-  // concurrent workgroups stream different DRAM regions (0: in order)
-  int krot;
-  // B is a tiled vocabulary head of 128 x 64 blocks (davet_pack_head).  1:
-  // BN = 128, BK = 64, tile (kt, nb) is the contiguous block at
-  // (kt * n_tiles_n + nb) * 8192.  2: BN a multiple of 128, BK 32 or 64: slab
-  // step kt reads BK columns of each of its BN / 128 blocks in chunk
-  // kt * BK / 64, from column kt * BK % 64.
+  // B is a tiled vocabulary head of 128 x 64 blocks (davet_pack_head), BN a
+  // multiple of 128, BK 32 or 64: slab step kt reads BK columns of each of
+  // its BN / 128 blocks in chunk kt * BK / 64, from column kt * BK % 64
   int b_tiled;
   // non-finite 16-bit values stored by EPI_STORE / EPI_SWIGLU (may be null)
   int32_t* overflow;
@@ -216,17 +207,14 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
     } else {
       gn = min(n0 + r, N - 1);
     }
-    if (ep.b_tiled == 2)
+    if (ep.b_tiled)
       b_src[q] = B + ((size_t)min(nb * (BN / 128) + (r >> 7), (N - 1) >> 7) * 128 +
                       (r & 127)) * 64 + c * 8;
     else
-      b_src[q] = ep.b_tiled
-                     ? B + ((size_t)kt0 * n_ntiles + nb) * BN * BK + (size_t)r * BK + c * 8
-                     : base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
+      b_src[q] = base + (size_t)gn * K + (size_t)kt0 * BK + c * 8;
   }
   const size_t b_kstride =
-      ep.b_tiled == 2 ? (size_t)((N + 127) / 128) * 128 * 64
-      : ep.b_tiled   ? (size_t)n_ntiles * BN * BK : (size_t)BK;
+      ep.b_tiled ? (size_t)((N + 127) / 128) * 128 * 64 : (size_t)BK;
 
   // A load instructions of this wave holding at least one live row: rows
   // past the last live one are not fetched (their LDS rows feed only output
@@ -235,18 +223,15 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   const int na = __builtin_amdgcn_readfirstlane(
       max(0, min(AI, (m_live - m0 - wave * AI * RPI + RPI - 1) / RPI)));
   const int lpt_live = na + BI;
-  const int rot = ep.krot ? (int)(((long)nb * ep.krot) % nk) : 0;
   auto issue = [&](int stage, int kt) {
-    kt += rot;
-    if (kt >= nk) kt -= nk;
     char* sa = smem + stage * S_BYTES;
     char* sb = sa + A_BYTES;
 #pragma unroll
     for (int q = 0; q < AI; ++q)
       if (q < na) dma16(a_src[q] + (size_t)kt * BK, sa + (wave * AI + q) * 1024);
     const int kel = (kt0 + kt) * BK;       // first K element of the slab
-    const size_t boff = ep.b_tiled == 2 ? (size_t)(kel >> 6) * b_kstride + (kel & 63)
-                                        : (size_t)kt * b_kstride;
+    const size_t boff = ep.b_tiled ? (size_t)(kel >> 6) * b_kstride + (kel & 63)
+                                   : (size_t)kt * b_kstride;
 #pragma unroll
     for (int q = 0; q < BI; ++q)
       dma16(b_src[q] + boff, sb + (wave * BI + q) * 1024);
@@ -514,44 +499,36 @@ int launch_tiles(const uint16_t* A, const uint16_t* B, const uint16_t* B2,
   return DAVET_OK;
 }
 
-// The kernel variants the planner can pick (index = GemmPlan::tile).
+// The kernel variants the planner can pick (index = GemmPlan::tile; the
+// indices are those of the measurement tables, other tiles measured slower).
 using V0 = Var<128, 128, 32, 4, 4>;    // 64 KB LDS, 2 workgroups per CU
-using V1 = Var<256, 128, 32, 4, 8>;
-using V2 = Var<128, 256, 32, 4, 8>;
-using V3 = Var<256, 256, 32, 4, 8>;    // large M
-using V4 = Var<128, 128, 64, 4, 4>;    // 128 KB LDS, deep 128-byte slabs
-using V5 = Var<64, 128, 32, 5, 4>;     // 60 KB: 2 workgroups per CU
 using V6 = Var<128, 128, 64, 2, 4>;    // 64 KB, 2 workgroups per CU
-using V7 = Var<256, 128, 64, 2, 8>;    // 96 KB
 using V8 = Var<256, 256, 64, 2, 8>;    // 128 KB, deep slabs, large M
-using V9 = Var<128, 256, 64, 2, 8>;    // 96 KB
-using V10 = Var<128, 128, 32, 3, 4>;   // 48 KB: 3 workgroups per CU
-using V11 = Var<128, 128, 32, 2, 4>;   // 32 KB
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
 using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
 // 192-row tiles: fewer padded rows and a fuller last wave of workgroups for
 // sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
 using V14 = Var<192, 128, 64, 2, 4>;   // 80 KB, 2 workgroups per CU
 using V15 = Var<128, 256, 32, 3, 8>;   // 72 KB: tiled vocabulary head
-constexpr int N_VARIANTS = 16;
 
 int variant_bn(int tile) {
   switch (tile) {
-    case 2: case 3: case 8: case 9: case 13: case 15: return 256;
+    case 8: case 13: case 15: return 256;
     default: return 128;
   }
 }
 int variant_bm(int tile) {
   switch (tile) {
     case 14: return 192;
-    case 1: case 3: case 7: case 8: case 13: return 256;
-    case 5: return 64;
+    case 8: case 13: return 256;
     default: return 128;
   }
 }
 int variant_bk(int tile) {
-  if (tile == 15) return 32;
-  return (tile == 4 || (tile >= 6 && tile <= 9) || tile >= 12) ? 64 : 32;
+  return (tile == 0 || tile == 15) ? 32 : 64;
+}
+bool variant_known(int tile) {
+  return tile == 0 || tile == 6 || tile == 8 || (tile >= 12 && tile <= 14);
 }
 
 template <typename Fmt, int EPI>
@@ -560,17 +537,8 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
                  hipStream_t s) {
 #define LV(Vn) return launch_tiles<Fmt, Vn, EPI>(A, B, B2, M, N, K, p.ksplit, ep, s)
   switch (p.tile) {
-    case 1: LV(V1);
-    case 2: LV(V2);
-    case 3: LV(V3);
-    case 4: LV(V4);
-    case 5: LV(V5);
     case 6: LV(V6);
-    case 7: LV(V7);
     case 8: LV(V8);
-    case 9: LV(V9);
-    case 10: LV(V10);
-    case 11: LV(V11);
     case 12: LV(V12);
     case 13: LV(V13);
     case 14: LV(V14);
@@ -620,13 +588,13 @@ constexpr int kNP = 26;
 struct TableShape { int N, K; GemmPlan plan[kNP]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4, 0}, {14, 2, 0}, {13, 2, 0}, {13, 2, 0}, {13, 2, 0}, {12, 1, 0}, {14, 2, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {14, 2, 0}, {14, 1, 0}, {12, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {12288, 4096, {{8, 4}, {14, 2}, {13, 2}, {13, 2}, {13, 2}, {12, 1}, {14, 2}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {14, 2}, {14, 1}, {12, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8, 0}, {6, 5, 0}, {6, 4, 0}, {6, 4, 0}, {12, 4, 0}, {6, 3, 0}, {14, 4, 0}, {12, 2, 0}, {6, 2, 0}, {6, 2, 0}, {8, 3, 0}, {14, 2, 0}, {14, 2, 0}, {12, 1, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {4096, 4096, {{6, 8}, {6, 5}, {6, 4}, {6, 4}, {12, 4}, {6, 3}, {14, 4}, {12, 2}, {6, 2}, {6, 2}, {8, 3}, {14, 2}, {14, 2}, {12, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {12, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {24576, 4096, {{8, 2}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {14, 1}, {13, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{12, 8, 0}, {14, 8, 0}, {14, 8, 0}, {8, 8, 0}, {8, 8, 0}, {6, 3, 0}, {13, 5, 0}, {14, 4, 0}, {13, 4, 0}, {8, 4, 0}, {13, 3, 0}, {14, 2, 0}, {14, 2, 0}, {13, 2, 0}, {8, 2, 0}, {8, 3, 0}, {14, 1, 0}, {14, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}, {13, 2, 0}, {13, 1, 0}, {13, 1, 0}, {13, 1, 0}}},
+    {4096, 12288, {{12, 8}, {14, 8}, {14, 8}, {8, 8}, {8, 8}, {6, 3}, {13, 5}, {14, 4}, {13, 4}, {8, 4}, {13, 3}, {14, 2}, {14, 2}, {13, 2}, {8, 2}, {8, 3}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 2}, {13, 1}, {13, 1}, {13, 1}}},
 };
 
 // Point i serves the rows up to the geometric mean of points i and i+1.
@@ -698,6 +666,8 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
   if (M <= 0) return DAVET_OK;
   if (plan.ksplit > 1 && (size_t)plan.ksplit * M * N * 4 > partial_cap)
     return set_error(DAVET_ENOMEM, "gemm16: split-K partials exceed the workspace");
+  if (!variant_known(plan.tile))
+    return set_error(DAVET_EINVAL, "gemm16: unknown tile variant");
   if (N % variant_bn(plan.tile) || K % variant_bk(plan.tile) ||
       (plan.ksplit > 1 && (K / variant_bk(plan.tile)) < plan.ksplit))
     return set_error(DAVET_ESHAPE, "gemm16: N or K not a multiple of the tile");
@@ -714,7 +684,6 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
   ep.part_ld = N;
   ep.dual = epi == EPI_SWIGLU;
   ep.ffn = N / 2;
-  ep.krot = plan.krot;
   ep.overflow = overflow;
   return dtype == DAVET_F16
              ? gemm_dispatch<F16>(plan, epi, A, B, B2, M, N, K, ep, s)
@@ -733,49 +702,42 @@ int launch_gemm16(int dtype, int epi, const GemmPlan& plan, const uint16_t* A,
 // 256 rows where V15's steps with every 128.  Both read the same columns per
 // lane, so logits and slab partials are the same bits whichever runs.  The
 // row-major layout takes 128 x 128 tiles with 8 wavefronts.
-static int head16_variant(int variant, int tiled, int live) {
-  if (variant >= 0) return variant;
+static int head16_variant(int tiled, int live) {
   if (!tiled) return 12;
   const int n128 = (std::max(live, 1) + 127) / 128;
   return (n128 == 1 || (n128 % 2 == 1 && n128 <= 5)) ? 15 : 13;
 }
 
-int head16_slabs(int vocab, int variant, int tiled, int live_bound) {
-  const int bn = variant_bn(head16_variant(variant, tiled, live_bound));
+int head16_slabs(int vocab, int tiled, int live_bound) {
+  const int bn = variant_bn(head16_variant(tiled, live_bound));
   return (vocab + bn - 1) / bn;
 }
 
 int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
                   const int32_t* list, int max_rows, int vocab, int d,
                   int mask_id, float* pmax, float* psum, int32_t* parg,
-                  float* logits_out, hipStream_t s, int variant, int krot,
-                  int tiled, int live_bound) {
+                  float* logits_out, hipStream_t s, int tiled,
+                  int live_bound) {
   // Row-major head: 8 wavefronts on the 128 x 128 tile (V12 over V6): the
   // matrix work of a slab is spread over twice the waves, so it hides behind
   // the other workgroup's stream (measured on MI355X: 201 -> 187 us at 2 live
   // rows, 214 -> 192 at 64)
   const int live = live_bound < 0 ? max_rows : std::min(max_rows, live_bound);
-  variant = head16_variant(variant, tiled, live);
-  // K-order rotation per vocabulary slab: helps the weight stream of an
-  // isolated head launch on MI355X but not inside the denoising step (the
-  // measured default there is 0, every slab starting at k = 0)
-  if (krot < 0) krot = DAVET_HEAD_KROT;
+  const int variant = head16_variant(tiled, live);
   if (d % BK_MIN) return set_error(DAVET_ESHAPE, "head16: d % 32 != 0");
   ProfScope ps(KC_HEAD, s);
   EpiArgs ep{};
   ep.list = list;
   ep.vocab = vocab;
   ep.mask_id = mask_id;
-  ep.n_slabs = head16_slabs(vocab, variant, tiled, live);
+  ep.n_slabs = head16_slabs(vocab, tiled, live);
   ep.pmax = pmax;
   ep.psum = psum;
   ep.parg = parg;
   ep.logits_out = logits_out;
-  ep.krot = krot;
-  const bool wide = variant == 8 || variant == 13 || variant == 15;
-  ep.b_tiled = tiled ? (wide ? 2 : 1) : 0;
-  if (tiled && ((variant != 6 && variant != 12 && !wide) || d % 64))
-    return set_error(DAVET_EINVAL, "head16: the tiled head needs 128 x 64 tiles");
+  ep.b_tiled = tiled;
+  if (tiled && d % 64)
+    return set_error(DAVET_EINVAL, "head16: the tiled head needs d % 64 == 0");
   // m_slots M slots per vocabulary slab: a workgroup loops over the live row
   // tiles mb, mb + m_slots, ...  m_slots covers live_bound, a bound on the
   // live rows the caller knows on the host (the schedule loop's: at most
@@ -788,11 +750,6 @@ int launch_head16(int dtype, const uint16_t* Hm, const uint16_t* W,
 #define HV(Fmt, Vn) return launch_tiles<Fmt, Vn, EPI_HEAD>(Hm, W, nullptr, max_rows, vocab, d, 1, ep, s, m_slots)
 #define HEAD_VARIANTS(Fmt)       \
   switch (variant) {             \
-    case 0: HV(Fmt, V0);         \
-    case 6: HV(Fmt, V6);         \
-    case 8: HV(Fmt, V8);         \
-    case 10: HV(Fmt, V10);       \
-    case 11: HV(Fmt, V11);       \
     case 12: HV(Fmt, V12);       \
     case 13: HV(Fmt, V13);       \
     case 15: HV(Fmt, V15);       \

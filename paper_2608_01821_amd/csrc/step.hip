@@ -397,13 +397,13 @@ int davet::denoise_step_impl(const davet_model_cfg* cfg, const davet_weights* w,
   if (bf) {
     const bool tiled = w->head_layout == DAVET_HEAD_TILED;
     const int live = std::max(1, std::min(rows, rows_bound));
-    const int slabs = head16_slabs(c.vocab, -1, tiled, live);
+    const int slabs = head16_slabs(c.vocab, tiled, live);
     float* pmax = reinterpret_cast<float*>(ws + lay.pmax);
     float* psum = reinterpret_cast<float*>(ws + lay.psum);
     int32_t* parg = reinterpret_cast<int32_t*>(ws + lay.parg);
     RUN(launch_head16(dt, (const uint16_t*)Hm, (const uint16_t*)w->head, list,
                       rows, c.vocab, d, c.mask_id, pmax, psum, parg,
-                      logits_out, s, -1, -1, tiled, live));
+                      logits_out, s, tiled, live));
     RUN(launch_head_merge(list, rows, slabs, pmax, psum, parg, conf_out,
                           argmax_out, s));
   } else {
