@@ -44,11 +44,13 @@ constexpr int BK_MIN = 32;   // K must be a multiple of this
 constexpr int EPI_HEAD = 3;
 
 // Kernel variants: tile BM x BN, K slab BK (64-byte or 128-byte LDS rows),
-// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2, 16: 8x2).
-template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_>
+// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2, 16: 8x2);
+// IGLP >= 0 asks the compiler's scheduler for its matrix-op interleaving
+// strategy of that number (__builtin_amdgcn_iglp_opt) on the slab body.
+template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_, int IGLP_ = -1>
 struct Var {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_,
-                       WAVES = WAVES_;
+                       WAVES = WAVES_, IGLP = IGLP_;
   static constexpr int LDS = STAGES * (BM + BN) * BK * 2;
   // workgroups per CU the register budget must allow (LDS is 160 KB per CU)
   static constexpr int MINB = LDS <= 80 * 1024 ? (LDS <= 53 * 1024 ? 3 : 2) : 1;
@@ -273,6 +275,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
         // 32-deep K steps of 16 x 16 x 32 matrix ops: lane l supplies row
         // (or column) l % 16 of a 16-row fragment and k = 8 (l / 16) .. +7,
         // i.e. 16-byte chunk 4 kk + l / 16 of that LDS row
+        if constexpr (V::IGLP >= 0) __builtin_amdgcn_iglp_opt(V::IGLP);
 #pragma unroll
         for (int kk = 0; kk < BK / 32; ++kk) {
           const int c = kk * 4 + k4;
@@ -502,13 +505,17 @@ int launch_tiles(const uint16_t* A, const uint16_t* B, const uint16_t* B2,
 // The kernel variants the planner can pick (index = GemmPlan::tile; the
 // indices are those of the measurement tables, other tiles measured slower).
 using V0 = Var<128, 128, 32, 4, 4>;    // 64 KB LDS, 2 workgroups per CU
-using V6 = Var<128, 128, 64, 2, 4>;    // 64 KB, 2 workgroups per CU
+// V6 and V14 with the scheduler's interleaving strategies 1 and 0: measured
+// on MI355X (candidates interleaved launch by launch, cold weights) never
+// slower on any table entry that uses them, median 5 % (V6) and 3.6 % (V14)
+// faster; the 256 x 256 and 8-wave 128 x 128 tiles gain nothing from it
+using V6 = Var<128, 128, 64, 2, 4, 1>; // 64 KB, 2 workgroups per CU
 using V8 = Var<256, 256, 64, 2, 8>;    // 128 KB, deep slabs, large M
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
 using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
 // 192-row tiles: fewer padded rows and a fuller last wave of workgroups for
 // sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
-using V14 = Var<192, 128, 64, 2, 4>;   // 80 KB, 2 workgroups per CU
+using V14 = Var<192, 128, 64, 2, 4, 0>; // 80 KB, 2 workgroups per CU
 using V15 = Var<128, 256, 32, 3, 8>;   // 72 KB: tiled vocabulary head
 
 int variant_bn(int tile) {
