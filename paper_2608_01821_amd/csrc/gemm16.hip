@@ -44,13 +44,15 @@ constexpr int BK_MIN = 32;   // K must be a multiple of this
 constexpr int EPI_HEAD = 3;
 
 // Kernel variants: tile BM x BN, K slab BK (64-byte or 128-byte LDS rows),
-// STAGES-deep LDS ring, WAVES wavefronts (4: 2x2 grid, 8: 4x2, 16: 8x2);
-// IGLP >= 0 asks the compiler's scheduler for its matrix-op interleaving
-// strategy of that number (__builtin_amdgcn_iglp_opt) on the slab body.
-template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_, int IGLP_ = -1>
+// STAGES-deep LDS ring, WAVES wavefronts in a (WAVES / WN) x WN grid (WN = 2
+// or 4 wave columns); IGLP >= 0 asks the compiler's scheduler for its
+// matrix-op interleaving strategy of that number (__builtin_amdgcn_iglp_opt)
+// on the slab body.
+template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_, int IGLP_ = -1,
+          int WN_ = 2>
 struct Var {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_,
-                       WAVES = WAVES_, IGLP = IGLP_;
+                       WAVES = WAVES_, IGLP = IGLP_, WN = WN_;
   static constexpr int LDS = STAGES * (BM + BN) * BK * 2;
   // workgroups per CU the register budget must allow (LDS is 160 KB per CU)
   static constexpr int MINB = LDS <= 80 * 1024 ? (LDS <= 53 * 1024 ? 3 : 2) : 1;
@@ -143,10 +145,17 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   using v8 = typename Fmt::v8;
   constexpr int BM = V::BM, BN = V::BN, BK = V::BK, STAGES = V::STAGES;
   constexpr int WAVES = V::WAVES;
-  constexpr int WM = WAVES / 2;          // wave grid WM x 2
+  constexpr int WN = V::WN;              // wave grid WM x WN
+  constexpr int WM = WAVES / WN;
   constexpr int WROWS = BM / WM;         // rows per wave
   constexpr int TM = WROWS / 32;         // 32-row sub-tiles per wave
-  constexpr int TN = BN / 64;            // 32-col sub-tiles per wave
+  constexpr int TN = BN / 64;            // 64-column groups of the tile
+  constexpr int CW = 64 / WN;            // a wave's columns in each group
+  constexpr int QC = CW / 16;            // ... as 16-column blocks
+  constexpr int NQ = 2 * QC;             // 16 x 16 accumulators per 32-row
+                                         // sub-tile and column group
+  static_assert(WN == 2 || WN == 4, "two or four wave columns");
+  static_assert(EPI != EPI_HEAD || WN == 2, "the head reduction pairs two wave columns");
   constexpr int CPR = BK / 8;            // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CPR;          // rows per load instruction
   constexpr int AI = BM / (RPI * WAVES); // A load instructions per wave/stage
@@ -181,7 +190,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   // wave-uniform values live in scalar registers (branches on them are
   // scalar, not exec-masked)
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int l32 = lane & 31, hh = lane >> 5;
   const int l16 = lane & 15, k4 = lane >> 4;
   const bool dual = (EPI == EPI_SWIGLU) || (EPI == EPI_PARTIAL && ep.dual);
@@ -239,15 +248,15 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
       dma16(b_src[q] + boff, sb + (wave * BI + q) * 1024);
   };
 
-  // acc[i][j][q]: the 16 x 16 block (q >> 1, q & 1) of the wave's 32 x 32
-  // block (i, j), one v_mfma_f32_16x16x32 accumulator each
-  f32x4 acc[TM][TN][4];
+  // acc[i][j][q]: the 16 x 16 block (q / QC, q % QC) of the wave's
+  // 32 x CW block (i, j), one v_mfma_f32_16x16x32 accumulator each
+  f32x4 acc[TM][TN][NQ];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[i][j][q][e] = 0.f;
 
@@ -279,7 +288,7 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
         for (int kk = 0; kk < BK / 32; ++kk) {
           const int c = kk * 4 + k4;
-          v8 af[NL][2], bfr[TN][2];
+          v8 af[NL][2], bfr[TN][QC];
 #pragma unroll
           for (int i = 0; i < NL; ++i)
 #pragma unroll
@@ -290,8 +299,8 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
           for (int j = 0; j < TN; ++j)
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const int r = j * 64 + wn * 32 + h * 16 + l16;
+            for (int h = 0; h < QC; ++h) {
+              const int r = j * 64 + wn * CW + h * 16 + l16;
               bfr[j][h] = *reinterpret_cast<const v8*>(sb + swz<BK>(r, c));
             }
 #pragma unroll
@@ -299,8 +308,8 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
             for (int j = 0; j < TN; ++j)
 #pragma unroll
-              for (int q = 0; q < 4; ++q)
-                acc[i][j][q] = Fmt::mfma16(af[i][q >> 1], bfr[j][q & 1],
+              for (int q = 0; q < NQ; ++q)
+                acc[i][j][q] = Fmt::mfma16(af[i][q / QC], bfr[j][q % QC],
                                            acc[i][j][q]);
         }
       }
@@ -316,9 +325,9 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
   }
 
   // ---------------------------------------------------------------- epilogue
-  // acc[i][j][q][u]: row = wm*WROWS + i*32 + (q>>1)*16 + (lane/16)*4 + t,
-  //                  col = j*64 + wn*32 + (q&1)*16 + lane%16   (tile-local)
-  // so a lane's column in each 64-column group j is wn*32 + (q&1)*16 + l16
+  // acc[i][j][q][u]: row = wm*WROWS + i*32 + (q/QC)*16 + (lane/16)*4 + u,
+  //                  col = j*64 + wn*CW + (q%QC)*16 + lane%16   (tile-local)
+  // so a lane's column in each 64-column group j is wn*CW + (q%QC)*16 + l16
   int nf = 0;     // non-finite 16-bit values stored by this lane
   const int rrow = k4 * 4;
   if constexpr (EPI == EPI_STORE) {
@@ -327,12 +336,12 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          const int row = m0 + wm * WROWS + i * 32 + (q / QC) * 16 + rrow + u;
           if (row >= M) continue;
-          const int cl = wn * 32 + (q & 1) * 16 + l16;
+          const int cl = wn * CW + (q % QC) * 16 + l16;
           uint16_t* crow = C + (size_t)row * ep.ldc + n0 + cl;
           if (rope) {
             // j even / j+1: dims cl and cl+64 of the head starting at n0 + j*64
@@ -360,12 +369,12 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          const int row = m0 + wm * WROWS + i * 32 + (q / QC) * 16 + rrow + u;
           if (row >= M) continue;
-          float* crow = C + (size_t)row * ep.ldc + n0 + wn * 32 + (q & 1) * 16 + l16;
+          float* crow = C + (size_t)row * ep.ldc + n0 + wn * CW + (q % QC) * 16 + l16;
 #pragma unroll
           for (int j = 0; j < TN; ++j) crow[j * 64] += acc[i][j][q][u];
         }
@@ -374,13 +383,13 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          const int row = m0 + wm * WROWS + i * 32 + (q / QC) * 16 + rrow + u;
           if (row >= M) continue;
-          uint16_t* crow = C + (size_t)row * ep.ldc + nb * (BN / 2) + wn * 32 +
-                           (q & 1) * 16 + l16;
+          uint16_t* crow = C + (size_t)row * ep.ldc + nb * (BN / 2) + wn * CW +
+                           (q % QC) * 16 + l16;
 #pragma unroll
           for (int j = 0; j < TN / 2; ++j) {
             const float g = acc[i][j][q][u], up = acc[i][j + TN / 2][q][u];
@@ -394,13 +403,13 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int row = m0 + wm * WROWS + i * 32 + (q >> 1) * 16 + rrow + u;
+          const int row = m0 + wm * WROWS + i * 32 + (q / QC) * 16 + rrow + u;
           if (row >= M) continue;
           float* prow = P + (size_t)row * ep.part_ld;
-          const int cl = wn * 32 + (q & 1) * 16 + l16;
+          const int cl = wn * CW + (q % QC) * 16 + l16;
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             int col;
@@ -517,17 +526,22 @@ using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
 // sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
 using V14 = Var<192, 128, 64, 2, 4, 0>; // 80 KB, 2 workgroups per CU
 using V15 = Var<128, 256, 32, 3, 8>;   // 72 KB: tiled vocabulary head
+// V13's tile with the 16 wavefronts in a 4 x 4 grid (64 x 64 per wave
+// instead of 32 x 128: a fifth fewer LDS fragment bytes per matrix op) and
+// the scheduler's interleaving strategy 0; same accumulation order per
+// output, so bit-identical to V13
+using V16 = Var<256, 256, 64, 2, 16, 0, 4>;
 
 int variant_bn(int tile) {
   switch (tile) {
-    case 8: case 13: case 15: return 256;
+    case 8: case 13: case 15: case 16: return 256;
     default: return 128;
   }
 }
 int variant_bm(int tile) {
   switch (tile) {
     case 14: return 192;
-    case 8: case 13: return 256;
+    case 8: case 13: case 16: return 256;
     default: return 128;
   }
 }
@@ -535,7 +549,8 @@ int variant_bk(int tile) {
   return (tile == 0 || tile == 15) ? 32 : 64;
 }
 bool variant_known(int tile) {
-  return tile == 0 || tile == 6 || tile == 8 || (tile >= 12 && tile <= 14);
+  return tile == 0 || tile == 6 || tile == 8 || (tile >= 12 && tile <= 14) ||
+         tile == 16;
 }
 
 template <typename Fmt, int EPI>
@@ -549,6 +564,7 @@ int launch_shape(const GemmPlan& p, const uint16_t* A, const uint16_t* B,
     case 12: LV(V12);
     case 13: LV(V13);
     case 14: LV(V14);
+    case 16: LV(V16);
     default: LV(V0);
   }
 #undef LV
@@ -583,7 +599,9 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 // shows, and was left out).  After the move to 16 x 16 x 32 matrix ops a
 // third sweep (variants 4, 6-9 and 12-14, splits 1-6 and 8, the split-K
 // reduction or the following norm included) changed thirteen entries whose
-// new plan was more than 4 % faster in each of three repetitions.
+// new plan was more than 4 % faster in each of three repetitions.  The
+// 4 x 4-wave tile (V16) then replaced V13 wherever it was not slower, timed
+// interleaved on every entry: median 5.8 % faster, bit-identical outputs.
 // Because the number of row tiles and of waves of workgroups changes in
 // steps, the best plan is jagged in M; a product of M rows takes the plan of
 // the nearest sample point in log M.
@@ -595,13 +613,13 @@ constexpr int kNP = 26;
 struct TableShape { int N, K; GemmPlan plan[kNP]; };
 constexpr TableShape kTable[] = {
     // QKV: N = 3d, K = d
-    {12288, 4096, {{8, 4}, {14, 2}, {13, 2}, {13, 2}, {13, 2}, {12, 1}, {14, 2}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {14, 2}, {14, 1}, {12, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}}},
+    {12288, 4096, {{8, 4}, {14, 2}, {13, 2}, {16, 2}, {16, 2}, {12, 1}, {14, 2}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {14, 2}, {14, 1}, {12, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // output projection: N = d, K = d
-    {4096, 4096, {{6, 8}, {6, 5}, {6, 4}, {6, 4}, {12, 4}, {6, 3}, {14, 4}, {12, 2}, {6, 2}, {6, 2}, {8, 3}, {14, 2}, {14, 2}, {12, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}}},
+    {4096, 4096, {{6, 8}, {6, 5}, {6, 4}, {6, 4}, {12, 4}, {6, 3}, {14, 4}, {12, 2}, {6, 2}, {6, 2}, {8, 3}, {14, 2}, {14, 2}, {12, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {14, 1}, {14, 1}, {14, 1}, {13, 1}, {14, 1}, {13, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}}},
+    {24576, 4096, {{8, 2}, {14, 1}, {14, 1}, {13, 1}, {16, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // down projection: N = d, K = ffn
-    {4096, 12288, {{12, 8}, {14, 8}, {14, 8}, {8, 8}, {8, 8}, {6, 3}, {13, 5}, {14, 4}, {13, 4}, {8, 4}, {13, 3}, {14, 2}, {14, 2}, {13, 2}, {8, 2}, {8, 3}, {14, 1}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 1}, {13, 2}, {13, 1}, {13, 1}, {13, 1}}},
+    {4096, 12288, {{12, 8}, {14, 8}, {14, 8}, {8, 8}, {8, 8}, {6, 3}, {16, 5}, {14, 4}, {13, 4}, {8, 4}, {16, 3}, {14, 2}, {14, 2}, {16, 2}, {8, 2}, {8, 3}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 2}, {16, 1}, {16, 1}, {16, 1}}},
 };
 
 // Point i serves the rows up to the geometric mean of points i and i+1.
@@ -625,12 +643,12 @@ static const TableShape* table_shape(int N, int K) {
 }
 
 // Other shapes: 128 x 128 tiles with 128-byte slabs and two workgroups per CU
-// up to ~2-3K rows, 256 x 256 tiles with 16 wavefronts above; narrow-N
+// up to ~2-3K rows, 256 x 256 tiles with 16 wavefronts (4 x 4) above; narrow-N
 // products split K until the grid fills the 256 CUs (tiles * ksplit < 512).
 static GemmPlan plan_generic(int M, int N, int K) {
   GemmPlan p{};
   const bool big = M >= (N >= 16384 ? 2048 : 3000);
-  p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 13 : (K % 64 == 0 ? 6 : 0);
+  p.tile = (big && N % 256 == 0 && K % 64 == 0) ? 16 : (K % 64 == 0 ? 6 : 0);
   const int bm = variant_bm(p.tile), bn = variant_bn(p.tile);
   const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int nk = K / variant_bk(p.tile);
