@@ -604,10 +604,12 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 // interleaved on every entry: median 5.8 % faster, bit-identical outputs.
 // A last interleaved sweep over the current variants (6, 8, 12, 13, 14, 16
 // with their scheduling hints, splits 1-6 and 8) moved 21 entries whose new
-// plan was at least 3 % faster.
+// plan was at least 3 % faster; a check of gate/up at 330-520 rows on two
+// parts then moved three more (192 x 128 at 356, 4 x 4-wave 256 x 256 at 420
+// and 480: 12 % and 6 % faster).
 // Because the number of row tiles and of waves of workgroups changes in
 // steps, the best plan is jagged in M; a product of M rows takes the plan of
-// the nearest sample point in log M.
+// the nearest sample point in log M, except in the ranges of kEdge.
 constexpr int kPointM[] = {209, 300, 356, 420, 480, 565, 650, 750, 889,
                            960, 1100, 1300, 1500, 1700, 2048, 2300, 2600,
                            2916, 3092, 3300, 3645, 3965, 5000, 8000, 12000,
@@ -620,9 +622,28 @@ constexpr TableShape kTable[] = {
     // output projection: N = d, K = d
     {4096, 4096, {{6, 8}, {6, 5}, {6, 4}, {6, 4}, {12, 4}, {6, 3}, {6, 2}, {12, 2}, {16, 4}, {6, 2}, {16, 3}, {14, 2}, {14, 2}, {16, 2}, {6, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2}, {14, 1}, {13, 1}, {13, 1}, {13, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
+    {24576, 4096, {{8, 2}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // down projection: N = d, K = ffn
     {4096, 12288, {{12, 8}, {14, 8}, {16, 8}, {16, 8}, {8, 8}, {16, 5}, {16, 5}, {8, 5}, {16, 4}, {16, 4}, {16, 3}, {14, 2}, {14, 2}, {16, 2}, {16, 2}, {8, 3}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 2}, {16, 1}, {16, 1}, {16, 1}}},
+};
+
+// Row counts just past a multiple of a point's tile height, where the point's
+// plan would add a nearly empty row tile the point itself does not have: the
+// plan measured there instead (each range timed at one row count inside it,
+// interleaved against the point's plan: 3-35 % faster; ranges where the next
+// point's plan was not faster keep the point's own).
+struct EdgeRange { int N, K, lo, hi; GemmPlan plan; };
+constexpr EdgeRange kEdge[] = {
+    {12288, 4096, 513, 520, {12, 1}},   {12288, 4096, 1537, 1596, {12, 1}},
+    {4096, 4096, 513, 520, {6, 3}},     {4096, 4096, 1025, 1027, {16, 3}},
+    {4096, 4096, 1537, 1596, {16, 2}},  {4096, 4096, 1793, 1865, {6, 1}},
+    {4096, 4096, 2049, 2170, {14, 1}},
+    {24576, 4096, 385, 386, {16, 1}},   {24576, 4096, 513, 520, {12, 1}},
+    {24576, 4096, 961, 1027, {16, 1}},  {24576, 4096, 1537, 1596, {16, 1}},
+    {24576, 4096, 2049, 2170, {14, 1}}, {24576, 4096, 2305, 2445, {16, 1}},
+    {4096, 12288, 513, 520, {16, 5}},   {4096, 12288, 769, 816, {16, 4}},
+    {4096, 12288, 1025, 1027, {16, 3}}, {4096, 12288, 1537, 1596, {16, 2}},
+    {4096, 12288, 2049, 2170, {16, 3}}, {4096, 12288, 4097, 4352, {16, 2}},
 };
 
 // Point i serves the rows up to the geometric mean of points i and i+1.
@@ -663,13 +684,18 @@ static GemmPlan plan_generic(int M, int N, int K) {
 }
 
 GemmPlan plan_gemm16(int M, int N, int K) {
-  if (const TableShape* t = table_shape(N, K)) return t->plan[point_index(M)];
+  if (const TableShape* t = table_shape(N, K)) {
+    for (const EdgeRange& e : kEdge)
+      if (e.N == N && e.K == K && M >= e.lo && M <= e.hi) return e.plan;
+    return t->plan[point_index(M)];
+  }
   return plan_generic(M, N, K);
 }
 
 // Largest split-K partial buffer (bytes) any M <= max_M needs.  Table shapes:
-// within the range a point serves the size grows with M, so the bound is
-// reached at the top of a range (or at max_M).  Other shapes: tiles * ksplit
+// within a run of rows that share one plan the size grows with M, so the
+// bound is reached at the top of a point's range, of an edge range or of the
+// rows below an edge range (or at max_M).  Other shapes: tiles * ksplit
 // < 512 caps it at 512 tiles of at most 256 x 256.
 size_t gemm16_partial_bound(int max_M, int N, int K) {
   size_t best = 0;
@@ -680,6 +706,11 @@ size_t gemm16_partial_bound(int max_M, int N, int K) {
   };
   if (table_shape(N, K)) {
     for (int i = 0; i < kNP; ++i) at(std::min(max_M, point_top(i)));
+    for (const EdgeRange& e : kEdge)
+      if (e.N == N && e.K == K) {
+        at(std::min(max_M, e.lo - 1));
+        at(std::min(max_M, e.hi));
+      }
     at(max_M);
     return best;
   }
