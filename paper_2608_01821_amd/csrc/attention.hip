@@ -70,6 +70,20 @@ __device__ __forceinline__ int v_slot(int r, int c) { return c ^ ((r & 3) << 2);
 
 // Workgroup barrier with no memory fence: each wave has waited for exactly
 // the loads it needs; the empty asm statements keep LDS accesses in place.
+// x combined with the value of lane l ^ 32: v_permlane32_swap exchanges the
+// upper half of one copy with the lower half of the other, so the two
+// results hold, in every lane, x of that lane and of its partner
+__device__ __forceinline__ float pair_max32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                                  __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                                  __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ void sync_lds() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -254,7 +268,7 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sc[mt][e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = pair_max32(tmax);
     // lazy maximum: keep m_run unless a score exceeds it by more than
     // 8 / scale_log2 (probabilities up to 2^8); the first tile always moves
     const float m_new =
@@ -272,7 +286,7 @@ attn16_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out,
         psum += p1;
         pw2[mt * 2 + (e >> 3)][(e & 7) >> 1] = Fmt::store2(p0, p1);
       }
-    psum += __shfl_xor(psum, 32, 64);
+    psum = pair_sum32(psum);
     l_run = l_run * alpha + psum;
     m_run = m_new;
     // rescale the accumulator unless no lane's maximum moved
