@@ -1,9 +1,9 @@
 // 16-bit (fp16 or bf16) matrix-core GEMMs of the denoiser: C[M,N] = A[M,K] B[N,K]^T
 // with both operands K-contiguous (activations row-major, weights [out, in]).
 //
-// CDNA4 design.  A workgroup of 4, 8 or 16 wavefronts (a WM x 2 grid) owns a
-// BM x BN tile; each wavefront accumulates (BM/WM) x (BN/2) with
-// v_mfma_f32_16x16x32 ops (fp32 accumulators).  K moves in slabs of BK (32
+// CDNA4 design.  A workgroup of 4, 8 or 16 wavefronts (a WM x WN grid, WN = 2
+// or 4) owns a BM x BN tile; each wavefront accumulates (BM/WM) x (BN/WN)
+// with v_mfma_f32_16x16x32 ops (fp32 accumulators).  K moves in slabs of BK (32
 // or 64) through a STAGES-deep ring of LDS stages filled by direct
 // global->LDS loads (global_load_lds_dwordx4: no VGPR staging), so up to
 // STAGES - 1 slabs are in flight while one feeds the matrix cores; one
