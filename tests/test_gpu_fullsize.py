@@ -105,6 +105,41 @@ def test_one_layer_full_size(one_layer, level, frac):
                   g_lg[0], 12, level)
 
 
+# Packed batches of copies of the workload's sample whose total token count
+# lies in the GEMM planner's edge ranges (row counts just past a multiple of a
+# tile height, which take a plan of their own instead of the nearest sample
+# point's): config -> [(levels of the packed sequences, total tokens)].
+EDGE_BATCHES = {
+    2: [([1, 1, 0, 0, 0, 0], 1548),   # QKV 128x128, out/down 256x256 2 splits
+        ([2, 2, 1], 2134),            # out 192x128, gate/up 192x128, down 3 splits
+        ([1, 0, 0, 0], 983),          # gate/up 256x256 (4 x 4 waves)
+        ([2, 2, 2, 2, 1, 0], 4121),   # down 256x256, 2 splits
+        ([0, 0, 1], 774)],            # down 256x256, 4 splits
+    3: [([1, 0], 1865),               # out 128x128 without a split
+        ([1, 0, 0], 2430)],           # gate/up 256x256 (4 x 4 waves)
+}
+
+
+def test_edge_plans_full_size(one_layer):
+    """The planner's edge-range plans in the packed step at the 8B shape: the
+    last sequence of each batch against the oracle (each sequence's result
+    depends on its own tokens only)."""
+    cfg, mdl, sample = one_layer
+    extra = len(sample.prompt) + cfg.resp_len
+    for k, (levels, total) in enumerate(EDGE_BATCHES[cfg.cid]):
+        assert sum(sample.sizes[lv] + extra for lv in levels) == total
+        rng = np.random.default_rng(70 + k)
+        st = [random_state(rng, cfg.resp_len, cfg.mask_id, cfg.vocab, 0.8)
+              for _ in levels]
+        ids = np.stack([a for a, _ in st])
+        masked = np.stack([m for _, m in st])
+        g_conf, g_am, g_lg = gpu_step(cfg, mdl, [sample] * len(levels),
+                                      levels, ids, masked)
+        i = len(levels) - 1
+        check_sampled(cfg, mdl, sample, levels[i], ids[i], masked[i],
+                      g_conf[i], g_am[i], g_lg[i], 4, 200 + k)
+
+
 def test_attention_split_matches_unsplit(one_layer):
     """The key-range split of attention at the 8B shape, against the same
     call with the split off (davet_set_attention_split(1)): logits of the
