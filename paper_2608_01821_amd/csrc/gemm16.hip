@@ -606,7 +606,8 @@ int gemm_dispatch(const GemmPlan& p, int epi, const uint16_t* A,
 // with their scheduling hints, splits 1-6 and 8) moved 21 entries whose new
 // plan was at least 3 % faster; a check of gate/up at 330-520 rows on two
 // parts then moved three more (192 x 128 at 356, 4 x 4-wave 256 x 256 at 420
-// and 480: 12 % and 6 % faster).
+// and 480: 12 % and 6 % faster), and one at 150-250 rows (8-wave 128 x 128
+// without a K split instead of 256 x 256 with two: 2-14 % faster).
 // Because the number of row tiles and of waves of workgroups changes in
 // steps, the best plan is jagged in M; a product of M rows takes the plan of
 // the nearest sample point in log M, except in the ranges of kEdge.
@@ -622,7 +623,7 @@ constexpr TableShape kTable[] = {
     // output projection: N = d, K = d
     {4096, 4096, {{6, 8}, {6, 5}, {6, 4}, {6, 4}, {12, 4}, {6, 3}, {6, 2}, {12, 2}, {16, 4}, {6, 2}, {16, 3}, {14, 2}, {14, 2}, {16, 2}, {6, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // gate + up: N = 2 ffn, K = d
-    {24576, 4096, {{8, 2}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
+    {24576, 4096, {{12, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {12, 1}, {14, 1}, {14, 1}, {14, 1}, {14, 1}, {16, 1}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}}},
     // down projection: N = d, K = ffn
     {4096, 12288, {{12, 8}, {14, 8}, {16, 8}, {16, 8}, {8, 8}, {16, 5}, {16, 5}, {8, 5}, {16, 4}, {16, 4}, {16, 3}, {14, 2}, {14, 2}, {16, 2}, {16, 2}, {8, 3}, {14, 1}, {14, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 1}, {16, 2}, {16, 1}, {16, 1}, {16, 1}}},
 };
