@@ -47,12 +47,14 @@ constexpr int EPI_HEAD = 3;
 // STAGES-deep LDS ring, WAVES wavefronts in a (WAVES / WN) x WN grid (WN = 2
 // or 4 wave columns); IGLP >= 0 asks the compiler's scheduler for its
 // matrix-op interleaving strategy of that number (__builtin_amdgcn_iglp_opt)
-// on the slab body.
+// on the slab body; SG = 1 gives it an explicit order instead (schedule
+// groups: the first 32-deep step's fragment reads, then the second step's
+// reads one per matrix op of the first step, then the remaining matrix ops).
 template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_, int IGLP_ = -1,
-          int WN_ = 2>
+          int WN_ = 2, int SG_ = 0>
 struct Var {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_,
-                       WAVES = WAVES_, IGLP = IGLP_, WN = WN_;
+                       WAVES = WAVES_, IGLP = IGLP_, WN = WN_, SG = SG_;
   static constexpr int LDS = STAGES * (BM + BN) * BK * 2;
   // workgroups per CU the register budget must allow (LDS is 160 KB per CU)
   static constexpr int MINB = LDS <= 80 * 1024 ? (LDS <= 53 * 1024 ? 3 : 2) : 1;
@@ -312,6 +314,20 @@ gemm16_kernel(const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
                 acc[i][j][q] = Fmt::mfma16(af[i][q / QC], bfr[j][q % QC],
                                            acc[i][j][q]);
         }
+        if constexpr (V::SG == 1) {
+          static_assert(BK == 64 && V::IGLP < 0, "two 32-deep steps, no strategy");
+          constexpr int DS_READ = 0x100, MATRIX = 0x008;   // group masks
+          constexpr int R = NL * 2 + TN * QC;   // fragment reads per step
+          constexpr int MO = NL * TN * NQ;      // matrix ops per step
+          static_assert(MO >= R, "a read per matrix op");
+          __builtin_amdgcn_sched_group_barrier(DS_READ, R, 0);
+#pragma unroll
+          for (int r = 0; r < R; ++r) {
+            __builtin_amdgcn_sched_group_barrier(DS_READ, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(MATRIX, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(MATRIX, 2 * MO - R, 0);
+        }
       }
     }
   };
@@ -514,17 +530,19 @@ int launch_tiles(const uint16_t* A, const uint16_t* B, const uint16_t* B2,
 // The kernel variants the planner can pick (index = GemmPlan::tile; the
 // indices are those of the measurement tables, other tiles measured slower).
 using V0 = Var<128, 128, 32, 4, 4>;    // 64 KB LDS, 2 workgroups per CU
-// V6 and V14 with the scheduler's interleaving strategies 1 and 0: measured
-// on MI355X (candidates interleaved launch by launch, cold weights) never
-// slower on any table entry that uses them, median 5 % (V6) and 3.6 % (V14)
-// faster; the 256 x 256 and 8-wave 128 x 128 tiles gain nothing from it
+// V6 with the scheduler's interleaving strategy 1: measured on MI355X
+// (candidates interleaved launch by launch, cold weights) never slower on any
+// table entry that uses it, median 5 % faster; the 256 x 256 and 8-wave
+// 128 x 128 tiles gain nothing from it.  V14 with explicit schedule groups
+// (SG = 1): 4-8 % faster than with strategy 0 on each of nine products at
+// 300-2916 rows, on three parts
 using V6 = Var<128, 128, 64, 2, 4, 1>; // 64 KB, 2 workgroups per CU
 using V8 = Var<256, 256, 64, 2, 8>;    // 128 KB, deep slabs, large M
 using V12 = Var<128, 128, 64, 2, 8>;   // 64 KB, 8 wavefronts, 2 WG/CU
 using V13 = Var<256, 256, 64, 2, 16>;  // 128 KB, 16 wavefronts
 // 192-row tiles: fewer padded rows and a fuller last wave of workgroups for
 // sequences of ~700-3000 tokens (3 sub-tiles of 32 rows per wave)
-using V14 = Var<192, 128, 64, 2, 4, 0>; // 80 KB, 2 workgroups per CU
+using V14 = Var<192, 128, 64, 2, 4, -1, 2, 1>; // 80 KB, 2 workgroups per CU
 using V15 = Var<128, 256, 32, 3, 8>;   // 72 KB: tiled vocabulary head
 // V13's tile with the 16 wavefronts in a 4 x 4 grid (64 x 64 per wave
 // instead of 32 x 128: a fifth fewer LDS fragment bytes per matrix op) and
