@@ -68,8 +68,6 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 __device__ __forceinline__ int k_slot(int r, int c) { return c ^ (r & 15); }
 __device__ __forceinline__ int v_slot(int r, int c) { return c ^ ((r & 3) << 2); }
 
-// Workgroup barrier with no memory fence: each wave has waited for exactly
-// the loads it needs; the empty asm statements keep LDS accesses in place.
 // x combined with the value of lane l ^ 32: v_permlane32_swap exchanges the
 // upper half of one copy with the lower half of the other, so the two
 // results hold, in every lane, x of that lane and of its partner
@@ -84,6 +82,8 @@ __device__ __forceinline__ float pair_sum32(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Workgroup barrier with no memory fence: each wave has waited for exactly
+// the loads it needs; the empty asm statements keep LDS accesses in place.
 __device__ __forceinline__ void sync_lds() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
